@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Throughput of the SOLO shared-readout local loss on one MI355X.
+
+One step = one call of the whole hot path (readout prep, row statistics, the
+local-loss pass of all K modules, module losses, the final module's
+readout-gradient pass and its gain reduction) over one batch of synthetic
+input already resident in HBM.  Default workload: the 1B-class shape
+(K=4 modules, T=16384 tokens = 8 x 2048 per module, d=2048, V=32000, bf16).
+
+Prints one JSON line (rank 0, N=1 only).  ``roofline`` is for the dominant
+kernel (the local-loss pass), timed live with HIP events recorded on the
+library's stream around that stage; ``cpu_baseline`` is the fp64 oracle on
+a bounded sample of the same workload, on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (256 CU x 4096 flop/clk x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0
+
+METRIC = "readout fwd+bwd tokens/sec and % of bf16 MFMA peak (1B-class, V=32000)"
+
+
+def _hip():
+    import torch  # noqa: F401  (same HIP runtime as torch)
+
+    lib = ctypes.CDLL("libamdhip64.so.7")
+    lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    return lib
+
+
+class EventSet:
+    """NUM_STAGES + 1 hipEvents per step: a start event and one after each stage."""
+
+    def __init__(self, hip, n):
+        self.hip = hip
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(e)) == 0
+            self.ev.append(e.value)
+
+    def elapsed(self, a, b) -> float:
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(self.ev[a]), ctypes.c_void_p(self.ev[b])) == 0
+        return float(ms.value)
+
+    def destroy(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
+    """fp64 oracle on the same workload restricted to sample_T tokens per module."""
+    import numpy as np
+
+    import oracle
+    from solo_inputs import make_inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"] or [0])
+    except Exception:
+        threads = 0
+    if not threads:
+        threads = len(os.sched_getaffinity(0))
+    x = make_inputs(cfg_name, seed=seed, T=sample_T)
+    h = x["h"].astype(np.float64)
+    W = x["W"].astype(np.float64)
+    g = x["gain"].astype(np.float64)
+    t0 = time.perf_counter()
+    oracle.readout_fwd_bwd(h, g, W, x["targets"], True)
+    dt = time.perf_counter() - t0
+    cfg = x["cfg"]
+    return {
+        "value": sample_T / dt,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{cfg_name} shape with T={sample_T} tokens per module (K={cfg.K}, d={cfg.d}, V={cfg.V}, "
+                  f"final-module dW included), fp64 NumPy oracle, {dt:.2f} s",
+        "seconds": dt,
+    }
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="1b", help="workload shape (solo_inputs.CONFIGS key)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=2048,
+                    help="tokens per module of the oracle's bounded sample (0 to skip)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_local_loss_1b.json"),
+                    help="HBM traffic of the dominant kernel measured with rocprofv3 counters (JSON), if present")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'How the path would "
+              "shard'); run with --gpus 1", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2609_35440_amd import binding, costmodel
+    from solo_inputs import make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    binding.load_library()
+    dev = torch.device("cuda:0")
+
+    x = make_inputs(args.config, seed=args.seed)
+    cfg = x["cfg"]
+    K, T, d, V = cfg.K, cfg.T, cfg.d, cfg.V
+    if cfg.dtype == "bf16":
+        def up(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(dev)
+
+        h, gain, W = up(x["h_bits"]), up(x["gain_bits"]), up(x["W_bits"])
+        elem = 2
+    else:
+        h, gain, W = (torch.from_numpy(x[k]).to(dev) for k in ("h", "gain", "W"))
+        elem = 4
+    targets = torch.from_numpy(x["targets"]).to(dev)
+    del x
+    dt = binding.SOLO_BF16 if cfg.dtype == "bf16" else binding.SOLO_F32
+    family = binding.kernel_family(K, T, d, V, dt)
+    out = binding.ReadoutResult(
+        losses=torch.empty(K, dtype=torch.float32, device=dev),
+        dh=torch.empty_like(h),
+        dW=torch.empty((V, d), dtype=torch.float32, device=dev),
+        dgain=torch.empty(d, dtype=torch.float32, device=dev),
+        row_loss=None,
+    )
+    ws = torch.empty(binding.workspace_size(K, T, d, V, dt, True), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    hip = _hip()
+    n_ev = binding.NUM_STAGES + 1
+    events = [EventSet(hip, n_ev) for _ in range(args.steps)]
+
+    def step(ev=None):
+        stage = None
+        if ev is not None:
+            assert hip.hipEventRecord(ctypes.c_void_p(ev.ev[0]), ctypes.c_void_p(stream.cuda_stream)) == 0
+            stage = ev.ev[1:]
+        binding.readout_fwd_bwd(h, gain, W, targets, True, 1e-6, workspace=ws, out=out, stream=stream,
+                                stage_events=stage)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    # per-step and per-stage times from the events (stage i ends at event i + 1)
+    step_ms = [e.elapsed(0, n_ev - 1) for e in events]
+    stage_ms = {name: float(np.mean([e.elapsed(i, i + 1) for e in events]))
+                for i, name in enumerate(binding.STAGE_NAMES)}
+    for e in events:
+        e.destroy()
+    ms_per_step = wall * 1e3 / args.steps
+    losses = out.losses.cpu().tolist()
+    if not all(np.isfinite(losses)):
+        print(f"non-finite losses {losses}", file=sys.stderr)
+        return 1
+
+    alg_flops = costmodel.readout_flops(K, T, V, d, True)
+    tokens_per_s = T / (ms_per_step / 1e3)
+    # dominant kernel: the local-loss pass, 2r per token of every module (logits + input gradient)
+    ll_ms = stage_ms["local_loss"]
+    ll_flops = 2 * 2 * K * T * V * d
+    achieved = ll_flops / (ll_ms / 1e3) / 1e12
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            with open(args.traffic) as f:
+                tr = json.load(f)
+            if tr.get("config") == args.config and tr.get("family") == family:
+                traffic = tr.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    result = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,1) hidden states, N(0,0.02^2) readout, 1+N(0,0.1^2) gain, Zipf(1.1) targets)",
+        "config": {"workload": f"{cfg.name}: K={K} modules, T={T} tokens/module, d={d}, V={V}, final-module dW",
+                   "K": K, "T": T, "d": d, "V": V, "kernel_family": family},
+        "tflops_algorithmic": alg_flops / (ms_per_step / 1e3) / 1e12,
+        "frac_bf16_peak_algorithmic": alg_flops / (ms_per_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+        "module_tokens_per_s": K * tokens_per_s,
+        "stage_ms": stage_ms,
+        "event_ms_per_step": float(np.median(step_ms)),
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "local-loss pass (logits + online log-sum-exp + dh), all K modules",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": ll_flops,
+            "launch_ms": ll_ms,
+        },
+        "losses": losses,
+    }
+    if args.cpu_sample_tokens > 0:
+        result["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample_tokens, args.seed)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -13,7 +13,8 @@ __all__ = ["costmodel", "readout_fwd_bwd", "workspace_size", "load_library", "So
 def __getattr__(name):
     # the binding loads the HIP library; import it only when asked for
     if name in ("readout_fwd_bwd", "workspace_size", "load_library", "SoloError", "binding"):
-        from . import binding
+        import importlib
 
+        binding = importlib.import_module(__name__ + ".binding")
         return binding if name == "binding" else getattr(binding, name)
     raise AttributeError(name)

@@ -1,0 +1,458 @@
+// Fused matrix-core passes of the SOLO shared-readout loss (bf16 operands, fp32
+// accumulate) for gfx950.
+//
+// Both passes have the shape "logit tile -> elementwise -> second product":
+//
+//   local-loss pass (every module, Eq. 2 and Eq. 3 of the paper):
+//     stationary X = 32 rows t of h_k, streamed Y = the readout rows v,
+//     z_tv = r_t <Wg_v, h_t>, online (max, sum-exp) per row, and
+//     acc_t += sum_v exp(z_tv - m_t) Wg_v        (Wg = W diag(gain))
+//     so that dn_t = (acc_t / s_t - Wg_{y_t}) / T at the end, followed by the
+//     RMSNorm backward.  The T x V logits and probabilities stay on chip.
+//
+//   readout-gradient pass (final module only; the copies get no gradient):
+//     stationary X = 32 readout rows v, streamed Y = the rows t of h_{K-1},
+//     delta_tv = (exp(z_tv - lse_t) - [v = y_t]) / T and
+//     D_v += sum_t delta_tv r_t h_t,  dW_v = gain * D_v,  dgain += W_v * D_v.
+//
+// Work split: a workgroup of 8 waves owns the 32 stationary rows; wave w owns
+// the d/8 columns [w d/8, (w+1) d/8).  Per chunk of 16 streamed rows, every
+// wave multiplies its column slice (split-K partial of the logit tile), the
+// partials meet in LDS, each wave finishes the elementwise step for 4 of the
+// 32 stationary rows, and every wave then accumulates its own column slice of
+// the second product.  The accumulator (32 rows x d/8 columns, fp32) and the
+// stationary operand stay in registers for the whole pass; the streamed
+// chunk goes HBM/L2 -> LDS directly and is read twice from LDS: row-wise for
+// the logit product and with the transposing read for the second product.
+#include "mfma_layout.h"
+#include "solo_internal.h"
+
+namespace solo {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr int NW = layout::NW;  // waves per workgroup
+constexpr int NTHR = NW * 64;
+constexpr int XR = kMfmaRows;  // stationary rows per workgroup (32)
+constexpr int YC = layout::YC;  // streamed rows per chunk
+constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: conflict-free 16 B writes
+constexpr float kLazyThresh = 8.0f;  // re-base the running max only when it grows by more than this
+
+template <int DS>
+struct Geo : layout::Geo<DS> {
+    static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
+    static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
+    static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
+    static constexpr int TOTAL = 2 * YBUF + NW * XR * PP * 4 + XR * YC * 2 + 2 * XR * 4 + NW * XR * 4;
+    static_assert(TOTAL <= 160 * 1024, "LDS budget");
+};
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(unsigned short u) {
+    return __uint_as_float(((unsigned)u) << 16);
+}
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Direct buffer -> LDS load of 16 bytes per lane; lane l's bytes land at
+// lds_base + 16 l.  Issued as inline asm so that the compiler does not track
+// it: the only reader of a chunk is the next step, which starts after an
+// explicit vmcnt(0) wait (wait_vm), and without tracking the compiler adds no
+// conservative waits before unrelated LDS accesses.
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, unsigned lds_base, int voffset) {
+    // one wait state between the M0 write and the LDS-DMA read of M0 (gfx9 hazard)
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(lds_base), "v"(voffset), "s"(rsrc)
+        : "memory", "m0");
+}
+
+__device__ __forceinline__ unsigned lds_addr(LDS_AS char* p) {
+    return __builtin_amdgcn_readfirstlane((unsigned)(unsigned long long)p);
+}
+
+// Buffer resource over [base, base + bytes): loads at or beyond `bytes`
+// return zeros, which pads the ragged last chunk.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, unsigned bytes) {
+    const unsigned long long a = (unsigned long long)base;
+    i32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)a);
+    r[1] = __builtin_amdgcn_readfirstlane((int)(unsigned)(a >> 32));
+    r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+    r[3] = 0x00020000;
+    return r;
+}
+
+// The direct-to-LDS stream of one chunk (layout in mfma_layout.h).
+template <int DS>
+struct ChunkStream {
+    using G = layout::Geo<DS>;
+    int voff[G::NV];
+
+    __device__ __forceinline__ void init(int d, int js, int lane) {
+#pragma unroll
+        for (int v = 0; v < G::NV; ++v) voff[v] = layout::stream_voff<DS>(v, d, js, lane);
+    }
+
+    // stream rows y0 .. y0 + 15 (this wave's DS columns) of Y into `slice`;
+    // rows at or beyond nY read as zeros
+    __device__ __forceinline__ void issue(const bf16* __restrict__ Y, int nY, int d, int y0, LDS_AS char* slice) const {
+#pragma unroll
+        for (int q = 0; q < G::NI; ++q) {
+            const int r0 = y0 + layout::stream_row0<DS>(q);
+            const int rows = nY - r0;
+            const unsigned rem = rows > 0 ? (unsigned)rows * (unsigned)d * 2u : 0u;
+            const i32x4 rsrc = make_rsrc(Y + (long long)r0 * d, rem);
+            buffer_load_lds16(rsrc, lds_addr(slice + layout::stream_lds_off<DS>(q)), voff[layout::stream_vidx<DS>(q)]);
+        }
+    }
+};
+
+// Barrier for LDS traffic only: unlike __syncthreads it does not drain the
+// in-flight chunk prefetch.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// MODE 0: local-loss pass, grid (ceil(T/32), K).
+// MODE 1: readout-gradient pass of module K-1, grid (ceil(V/32)).
+template <int MODE, int DS>
+__global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
+    using G = Geo<DS>;
+    // Separate LDS objects, so that the compiler can tell the chunk being read
+    // from the chunk being prefetched (no needless waits on the prefetch).
+    __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
+    __shared__ __attribute__((aligned(16))) char ybufB[G::YBUF];
+    __shared__ __attribute__((aligned(16))) float part[NW * XR * PP];
+    __shared__ __attribute__((aligned(16))) bf16 gbuf[XR * YC];
+    __shared__ float abuf[XR];
+    __shared__ float sbuf[XR];
+    __shared__ float cbuf[NW * XR];
+
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int d = a.d;
+    const int js = w * DS;
+    const int x0 = blockIdx.x * XR;
+    const int k = (MODE == 0) ? (int)blockIdx.y : a.K - 1;
+    const long long modoff = (long long)k * a.T;
+
+    const bf16* __restrict__ hk = (const bf16*)a.h + modoff * d;
+    const bf16* __restrict__ Wg = (const bf16*)a.Wg;
+    const bf16* __restrict__ X = (MODE == 0) ? hk : Wg;
+    const bf16* __restrict__ Y = (MODE == 0) ? Wg : hk;
+    const int nX = (MODE == 0) ? a.T : a.V;
+    const int nY = (MODE == 0) ? a.V : a.T;
+    const int nchunks = (nY + YC - 1) / YC;
+
+    LDS_AS char* sliceA = (LDS_AS char*)(LDS_AS void*)ybufA + w * G::SLICE;
+    LDS_AS char* sliceB = (LDS_AS char*)(LDS_AS void*)ybufB + w * G::SLICE;
+
+    // per-lane scalars of the rows this wave finishes in the elementwise step
+    const int xo = 4 * w + (lane >> 4);   // stationary row (0..31) owned in the elementwise step
+    const int yy = lane & 15;             // streamed row within the chunk
+    float own_r = 0.f;                    // MODE 0: r_t of row xo
+    int own_tgt = -1;                     // MODE 0: target of row xo
+    if (MODE == 0 && x0 + xo < nX) {
+        own_r = a.rstd[modoff + x0 + xo];
+        own_tgt = a.targets[modoff + x0 + xo];
+    }
+
+    ChunkStream<DS> stream;
+    stream.init(d, js, lane);
+    // first chunk in flight before the stationary operand is read
+    stream.issue(Y, nY, d, 0, sliceA);
+    float nx_r = 0.f, nx_lse = 0.f;
+    int nx_tgt = -1;
+    if (MODE == 1 && yy < nY) {
+        nx_r = a.rstd[modoff + yy];
+        nx_lse = a.lse[modoff + yy];
+        nx_tgt = a.targets[modoff + yy];
+    }
+
+    // stationary operand: B of the 16x16x32 logit product, lane holds
+    // X[x0 + 16 xb + lane%16][js + 32 kk + 8 (lane/16) .. +7]
+    bf16x8 xr[2][G::NK];
+#pragma unroll
+    for (int xb = 0; xb < 2; ++xb) {
+        const int xrow = x0 + 16 * xb + (lane & 15);
+#pragma unroll
+        for (int kk = 0; kk < G::NK; ++kk) {
+            if (xrow < nX) {
+                xr[xb][kk] = *(const bf16x8*)(X + (long long)xrow * d + js + 32 * kk + 8 * (lane >> 4));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xr[xb][kk][e] = (bf16)0.f;
+            }
+        }
+    }
+
+    f32x16 acc[G::NB];
+#pragma unroll
+    for (int b = 0; b < G::NB; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[b][i] = 0.f;
+
+    // online softmax state (MODE 0), per lane: row xo, streamed column yy
+    float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
+
+    // per-lane parts of the LDS addresses; the unrolled loops add 64 * kk or 64 * b
+    const int a_off = layout::rowread_off<DS>(lane);
+    const int c_lo = layout::trread_off<DS>(lane, 0);
+    const int c_hi = layout::trread_off<DS>(lane, 1);
+
+    auto step = [&](LDS_AS char* cur, LDS_AS char* nxt, int c) __attribute__((always_inline)) {
+        const int y0 = c * YC;
+        const float cur_r = nx_r, cur_lse = nx_lse;
+        const int cur_tgt = nx_tgt;
+        if (c + 1 < nchunks) {
+            stream.issue(Y, nY, d, y0 + YC, nxt);
+            if (MODE == 1) {
+                const int yn = y0 + YC + yy;
+                if (yn < nY) {
+                    nx_r = a.rstd[modoff + yn];
+                    nx_lse = a.lse[modoff + yn];
+                    nx_tgt = a.targets[modoff + yn];
+                }
+            }
+        }
+
+        // ---- split-K partial of the logit tile S[y][x] over this wave's columns
+        f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < G::NK; ++kk) {
+            const bf16x8 ay = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
+            S0 = mfma16(ay, xr[0][kk], S0);
+            S1 = mfma16(ay, xr[1][kk], S1);
+        }
+        // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
+        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
+        *(f32x4*)(part + (w * XR + 16 + (lane & 15)) * PP + 4 * (lane >> 4)) = S1;
+        lds_barrier();
+
+        // ---- elementwise step for rows xo = 4w .. 4w+3 (lane: row xo, column yy)
+        float sxy = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) sxy += part[(ww * XR + xo) * PP + yy];
+        const int yg = y0 + yy;
+        float gval;
+        if (MODE == 0) {
+            const bool yok = yg < nY;
+            const float z = yok ? sxy * own_r : -INFINITY;
+            float cmax = z;
+            cmax = fmaxf(cmax, __shfl_xor(cmax, 1, 64));
+            cmax = fmaxf(cmax, __shfl_xor(cmax, 2, 64));
+            cmax = fmaxf(cmax, __shfl_xor(cmax, 4, 64));
+            cmax = fmaxf(cmax, __shfl_xor(cmax, 8, 64));
+            float alpha = 1.f;
+            if (cmax > m_run + kLazyThresh) {
+                alpha = __expf(m_run - cmax);
+                s_part *= alpha;
+                m_run = cmax;
+            }
+            const float p = yok ? __expf(z - m_run) : 0.f;
+            s_part += p;
+            if (yg == own_tgt) zy_part = z;
+            gval = p;
+            if (yy == 0) abuf[xo] = alpha;
+        } else {
+            const int xg = x0 + xo;
+            gval = 0.f;
+            if (yg < nY && xg < nX) {
+                const float z = sxy * cur_r;
+                const float p = __expf(z - cur_lse);
+                gval = (p - (cur_tgt == xg ? 1.f : 0.f)) * cur_r * a.inv_T;
+            }
+        }
+        gbuf[xo * YC + yy] = (bf16)gval;
+        lds_barrier();
+
+        // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
+        const bf16x8 gfrag = *(bf16x8*)(gbuf + (lane & 31) * YC + 8 * (lane >> 5));
+        if (MODE == 0) {
+            const float al = abuf[lane & 31];
+            if (__any(al != 1.f)) {
+#pragma unroll
+                for (int b = 0; b < G::NB; ++b)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) acc[b][i] *= al;
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < G::NB; ++b) {
+            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_lo + 64 * b));
+            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_hi + 64 * b));
+            bf16x8 ay;
+            ay[0] = lo[0]; ay[1] = lo[1]; ay[2] = lo[2]; ay[3] = lo[3];
+            ay[4] = hi[0]; ay[5] = hi[1]; ay[6] = hi[2]; ay[7] = hi[3];
+            acc[b] = mfma32(ay, gfrag, acc[b]);
+        }
+        wait_vm();
+    };
+
+    wait_vm();
+    for (int c = 0; c < nchunks; c += 2) {
+        step(sliceA, sliceB, c);
+        if (c + 1 < nchunks) step(sliceB, sliceA, c + 1);
+    }
+
+    // ---- epilogues.  acc[b] lane layout: x = lane%32,
+    //      j = js + 32 b + 8 (i/4) + 4 (lane/32) + i%4 for i = 0..15
+    const int ex = lane & 31;
+    const int ehh = lane >> 5;
+    if (MODE == 0) {
+        // finish the online softmax of rows 4w..4w+3
+        float s = s_part, zy = zy_part;
+        s += __shfl_xor(s, 1, 64); s += __shfl_xor(s, 2, 64); s += __shfl_xor(s, 4, 64); s += __shfl_xor(s, 8, 64);
+        zy += __shfl_xor(zy, 1, 64); zy += __shfl_xor(zy, 2, 64); zy += __shfl_xor(zy, 4, 64); zy += __shfl_xor(zy, 8, 64);
+        if (yy == 0) {
+            const float lse = m_run + logf(s);
+            const bool tok = own_tgt >= 0 && own_tgt < nY;
+            const float rl = tok ? lse - zy : __int_as_float(0x7fc00000);
+            if (x0 + xo < nX) {
+                a.lse[modoff + x0 + xo] = lse;
+                a.rowloss[modoff + x0 + xo] = rl;
+            }
+            sbuf[xo] = 1.f / s;
+        }
+        __syncthreads();
+
+        const int xg = x0 + ex;
+        const bool xok = xg < nX;
+        const float rx = xok ? a.rstd[modoff + xg] : 0.f;
+        const int tgt = xok ? a.targets[modoff + xg] : -1;
+        const bool tok = tgt >= 0 && tgt < nY;
+        const float inv_s = sbuf[ex];
+        const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
+        const bf16* wrow = Wg + (long long)(tok ? tgt : 0) * d;
+        float cp = 0.f;
+#pragma unroll
+        for (int b = 0; b < G::NB; ++b) {
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+                const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                u16x4 hv = {0, 0, 0, 0}, wv = {0, 0, 0, 0};
+                if (xok) hv = *(const u16x4*)(hrow + j);
+                if (tok) wv = *(const u16x4*)(wrow + j);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float dn = (acc[b][4 * i4 + e] * inv_s - bf16_bits_to_f32(wv[e])) * a.inv_T;
+                    cp += dn * (rx * bf16_bits_to_f32(hv[e]));
+                    acc[b][4 * i4 + e] = dn;
+                }
+            }
+        }
+        cp += __shfl_xor(cp, 32, 64);
+        if (ehh == 0) cbuf[w * XR + ex] = cp;
+        __syncthreads();
+        float csum = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + ex];
+        const float cmean = csum / (float)d;
+        if (xok) {
+            bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b) {
+#pragma unroll
+                for (int i4 = 0; i4 < 4; ++i4) {
+                    const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                    const u16x4 hv = *(const u16x4*)(hrow + j);
+                    bf16x4 o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float n = rx * bf16_bits_to_f32(hv[e]);
+                        o[e] = (bf16)(rx * (acc[b][4 * i4 + e] - cmean * n));
+                    }
+                    *(bf16x4*)(dhrow + j) = o;
+                }
+            }
+        }
+    } else {
+        const int v = x0 + ex;
+        const bool vok = v < nX;
+        const bf16* wrow = (const bf16*)a.W + (long long)(vok ? v : 0) * d;
+        const bf16* gain = (const bf16*)a.gain;
+        float* dwrow = a.dW + (long long)(vok ? v : 0) * d;
+        float* dgp = a.dgain_part + (long long)blockIdx.x * d;
+#pragma unroll
+        for (int b = 0; b < G::NB; ++b) {
+#pragma unroll
+            for (int i4 = 0; i4 < 4; ++i4) {
+                const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                const u16x4 gv = *(const u16x4*)(gain + j);
+                u16x4 wv = {0, 0, 0, 0};
+                if (vok) wv = *(const u16x4*)(wrow + j);
+                f32x4 o;
+                float pr[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float D = acc[b][4 * i4 + e];
+                    o[e] = bf16_bits_to_f32(gv[e]) * D;
+                    pr[e] = bf16_bits_to_f32(wv[e]) * D;
+                }
+                if (vok) *(f32x4*)(dwrow + j) = o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float t = pr[e];
+                    t += __shfl_xor(t, 1, 64);
+                    t += __shfl_xor(t, 2, 64);
+                    t += __shfl_xor(t, 4, 64);
+                    t += __shfl_xor(t, 8, 64);
+                    t += __shfl_xor(t, 16, 64);
+                    pr[e] = t;
+                }
+                if (ex == 0) {
+                    f32x4 pv = {pr[0], pr[1], pr[2], pr[3]};
+                    *(f32x4*)(dgp + j) = pv;
+                }
+            }
+        }
+    }
+}
+
+template <int MODE, int DS>
+hipError_t launch_ds(const FusedArgs& a, hipStream_t s) {
+    dim3 grid = (MODE == 0) ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K) : dim3((unsigned)((a.V + XR - 1) / XR));
+    hipLaunchKernelGGL((k_fused<MODE, DS>), grid, dim3(NTHR), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_mode(const FusedArgs& a, hipStream_t s) {
+    switch (a.d / NW) {
+        case 32: return launch_ds<MODE, 32>(a, s);
+        case 64: return launch_ds<MODE, 64>(a, s);
+        case 96: return launch_ds<MODE, 96>(a, s);
+        case 128: return launch_ds<MODE, 128>(a, s);
+        case 160: return launch_ds<MODE, 160>(a, s);
+        case 192: return launch_ds<MODE, 192>(a, s);
+        case 224: return launch_ds<MODE, 224>(a, s);
+        case 256: return launch_ds<MODE, 256>(a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool mfma_supported(int dtype, int d) { return dtype == 0 && d % (NW * 32) == 0 && d >= NW * 32 && d <= NW * 256; }
+
+hipError_t launch_local_loss_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<0>(a, s); }
+hipError_t launch_readout_grad_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<1>(a, s); }
+
+}  // namespace solo

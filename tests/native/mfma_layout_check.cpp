@@ -1,0 +1,107 @@
+// Host check of the LDS layout used by the matrix-core passes: emulate the
+// direct-to-LDS stream of one chunk slice with the functions of
+// mfma_layout.h, then every row-wise and transposing operand read, and check
+// that each returns the element its MFMA operand needs.  Also counts LDS bank
+// conflicts (64 banks of 4 bytes) of both read patterns.
+// Transposing read semantics (ds_read_b64_tr_b16, per 16-lane group): lane i
+// receives, as element y, the 16-bit value (i % 4) of the 8 bytes addressed by
+// lane 4 y + i / 4 of its group.
+#include <cstdio>
+#include <map>
+#include <set>
+#include <utility>
+#include <vector>
+
+#include "mfma_layout.h"
+
+using namespace solo::layout;
+
+template <int DS>
+int check(int& conflicts_row, int& conflicts_tr) {
+    using G = Geo<DS>;
+    const int d = DS * NW;
+    int errors = 0;
+    conflicts_row = conflicts_tr = 0;
+    for (int w = 0; w < NW; ++w) {
+        const int js = w * DS;
+        // LDS byte -> (row, column) of the bf16 element stored there
+        std::map<int, std::pair<int, int>> lds;
+        for (int q = 0; q < G::NI; ++q) {
+            for (int lane = 0; lane < 64; ++lane) {
+                const int elem = stream_row0<DS>(q) * d + stream_voff<DS>(stream_vidx<DS>(q), d, js, lane) / 2;
+                const int row = elem / d, col = elem % d;
+                const int addr = stream_lds_off<DS>(q) + 16 * lane;
+                if (addr < 0 || addr + 16 > G::SLICE) ++errors;
+                for (int e = 0; e < 8; ++e) {
+                    if (lds.count(addr + 2 * e)) ++errors;  // two granules written to one place
+                    lds[addr + 2 * e] = {row, col + e};
+                }
+            }
+        }
+        if ((int)lds.size() != 16 * DS) ++errors;  // every element of the 16 x DS slice exactly once
+        // row-wise reads: lane -> row lane % 16, columns js + 32 kk + 8 (lane / 16) + e
+        for (int kk = 0; kk < DS / 32; ++kk) {
+            for (int g16 = 0; g16 < 4; ++g16) {
+                std::set<int> slots;
+                for (int l = 16 * g16; l < 16 * g16 + 16; ++l) {
+                    const int base = rowread_off<DS>(l) + 64 * kk;
+                    slots.insert((base / 16) % 16);
+                    for (int e = 0; e < 8; ++e) {
+                        auto it = lds.find(base + 2 * e);
+                        std::pair<int, int> want{l & 15, js + 32 * kk + 8 * (l >> 4) + e};
+                        if (it == lds.end() || it->second != want) ++errors;
+                    }
+                }
+                conflicts_row += 16 - (int)slots.size();
+            }
+        }
+        // transposing reads of block b: lane -> m = column js + 32 b + lane % 32,
+        // k = rows 8 (lane / 32) + 4 half + y
+        for (int b = 0; b < DS / 32; ++b) {
+            for (int half = 0; half < 2; ++half) {
+                int addr[64];
+                for (int l = 0; l < 64; ++l) addr[l] = trread_off<DS>(l, half) + 64 * b;
+                for (int h32 = 0; h32 < 2; ++h32) {
+                    std::set<int> banks;
+                    for (int l = 32 * h32; l < 32 * h32 + 32; ++l) {
+                        banks.insert((addr[l] / 4) % 64);
+                        banks.insert((addr[l] / 4 + 1) % 64);
+                    }
+                    conflicts_tr += 64 - (int)banks.size();
+                }
+                for (int l = 0; l < 64; ++l) {
+                    const int grp = l / 16, i = l % 16;
+                    for (int y = 0; y < 4; ++y) {
+                        const int src = grp * 16 + 4 * y + i / 4;
+                        auto it = lds.find(addr[src] + 2 * (i % 4));
+                        std::pair<int, int> want{8 * (l >> 5) + 4 * half + y, js + 32 * b + (l % 32)};
+                        if (it == lds.end() || it->second != want) ++errors;
+                    }
+                }
+            }
+        }
+    }
+    return errors;
+}
+
+template <int DS>
+int report() {
+    int cr = 0, ct = 0;
+    const int e = check<DS>(cr, ct);
+    std::printf("DS=%d padded=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d\n", DS, (int)Geo<DS>::PADDED,
+                Geo<DS>::SLICE, e, cr, ct);
+    return e;
+}
+
+int main() {
+    int e = 0;
+    e += report<32>();
+    e += report<64>();
+    e += report<96>();
+    e += report<128>();
+    e += report<160>();
+    e += report<192>();
+    e += report<224>();
+    e += report<256>();
+    return e == 0 ? 0 : 1;
+}

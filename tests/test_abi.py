@@ -1,0 +1,133 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, sizes its workspace without a T*V term, and rejects bad arguments
+on the host before any launch (these calls never reach the GPU)."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+from paper_2609_35440_amd import binding as B
+
+LIB = B.library_path()
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="library not built (run __graft_entry__.build())")
+
+# fake, aligned, never dereferenced: every call below fails validation first
+P = 0x10000
+WS = 1 << 40
+
+
+def call(**kw):
+    args = dict(K=2, T=8, d=64, V=32, dtype=B.SOLO_BF16, eps=1e-6, h=P, gain=P, W=P, targets=P, final_module_dW=1,
+                losses=P, row_loss=0, dh=P, dW=P, dgain=P, workspace=P, workspace_bytes=WS, stream=0)
+    args.update(kw)
+    return B.readout_fwd_bwd_raw(**args)
+
+
+def test_exports_match_header():
+    names = B.header_functions()
+    assert set(names) == {"solo_readout_abi_version", "solo_status_string", "solo_readout_workspace_size",
+                          "solo_readout_kernel_family", "solo_readout_fwd_bwd", "solo_readout_fwd_bwd_profiled"}
+    lib = ctypes.CDLL(LIB)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    assert set(names) <= exported
+    assert B.abi_version() == 1
+
+
+def test_status_strings():
+    for name, code in B.STATUS.items():
+        s = B.status_string(code)
+        assert isinstance(s, str) and s
+    assert B.status_string(99) == "unknown status"
+
+
+def test_workspace_has_no_TV_term():
+    # bf16 matrix-core family: Wg (V d 2) + rstd, lse, row_loss (3 K T 4) + dgain partials (ceil(V/32) d 4)
+    def al(x):
+        return (x + 255) // 256 * 256
+
+    for K, T, d, V in [(4, 16384, 2048, 32000), (2, 32768, 2048, 128256), (4, 8192, 1024, 32000), (1, 1, 256, 1)]:
+        want = al(V * d * 2) + 3 * al(K * T * 4) + al(-(-V // 32) * d * 4)
+        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, True) == want
+        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == al(V * d * 2) + 3 * al(K * T * 4)
+    # doubling T with V fixed grows the workspace by K*T*12 bytes only
+    a = B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True)
+    b = B.workspace_size(4, 32768, 2048, 32000, B.SOLO_BF16, True)
+    assert b - a == 3 * 4 * 16384 * 4
+    # far below one module's T x V fp32 logits (2.1 GB at the 1B shape)
+    assert a < 16384 * 32000 * 4 / 4
+    # invalid arguments -> 0
+    assert B.workspace_size(0, 8, 64, 32, B.SOLO_BF16, True) == 0
+    assert B.workspace_size(1, 8, 63, 32, B.SOLO_BF16, True) == 0
+    assert B.workspace_size(1, 8, 64, 32, 7, True) == 0
+    assert B.workspace_size(1, 8, 64, 32, B.SOLO_BF16, 2) == 0
+
+
+def test_kernel_family():
+    assert B.kernel_family(4, 16384, 2048, 32000, B.SOLO_BF16) == "mfma"
+    assert B.kernel_family(4, 8192, 1024, 32000, B.SOLO_BF16) == "mfma"
+    assert B.kernel_family(2, 256, 64, 512, B.SOLO_F32) == "valu"
+    assert B.kernel_family(8, 16384, 2560, 32000, B.SOLO_BF16) == "valu"
+    assert B.kernel_family(1, 1, 72, 3, B.SOLO_BF16) == "valu"
+    assert B.kernel_family(0, 1, 64, 3, B.SOLO_BF16) == "invalid"
+
+
+def test_profiled_entry_point_validates_identically():
+    # same host checks; stage events are never touched on an argument error
+    for kw, code in [(dict(K=0), "SOLO_ERR_SHAPE"), (dict(h=0), "SOLO_ERR_NULL"), (dict(workspace_bytes=1), "SOLO_ERR_WORKSPACE")]:
+        assert call(stage_events=[0x1234] * B.NUM_STAGES, **kw) == B.STATUS[code]
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=2), "SOLO_ERR_DTYPE"),
+    (dict(dtype=-1), "SOLO_ERR_DTYPE"),
+    (dict(K=0), "SOLO_ERR_SHAPE"),
+    (dict(T=0), "SOLO_ERR_SHAPE"),
+    (dict(V=0), "SOLO_ERR_SHAPE"),
+    (dict(d=0), "SOLO_ERR_SHAPE"),
+    (dict(d=60), "SOLO_ERR_SHAPE"),
+    (dict(d=4104), "SOLO_ERR_SHAPE"),
+    (dict(K=70000), "SOLO_ERR_SHAPE"),
+    (dict(K=65535, T=1 << 30), "SOLO_ERR_SHAPE"),
+    (dict(eps=-1.0), "SOLO_ERR_ARG"),
+    (dict(eps=float("nan")), "SOLO_ERR_ARG"),
+    (dict(eps=float("inf")), "SOLO_ERR_ARG"),
+    (dict(final_module_dW=2), "SOLO_ERR_ARG"),
+    (dict(h=0), "SOLO_ERR_NULL"),
+    (dict(gain=0), "SOLO_ERR_NULL"),
+    (dict(W=0), "SOLO_ERR_NULL"),
+    (dict(targets=0), "SOLO_ERR_NULL"),
+    (dict(losses=0), "SOLO_ERR_NULL"),
+    (dict(dh=0), "SOLO_ERR_NULL"),
+    (dict(workspace=0), "SOLO_ERR_NULL"),
+    (dict(dW=0), "SOLO_ERR_NULL"),
+    (dict(dgain=0), "SOLO_ERR_NULL"),
+    (dict(h=P + 8), "SOLO_ERR_ALIGN"),
+    (dict(W=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(gain=P + 4), "SOLO_ERR_ALIGN"),
+    (dict(dh=P + 8), "SOLO_ERR_ALIGN"),
+    (dict(targets=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(losses=P + 1), "SOLO_ERR_ALIGN"),
+    (dict(row_loss=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(workspace=P + 128), "SOLO_ERR_ALIGN"),
+    (dict(dW=P + 4), "SOLO_ERR_ALIGN"),
+    (dict(dgain=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(workspace_bytes=1000), "SOLO_ERR_WORKSPACE"),
+])
+def test_validation_errors(kw, code):
+    assert call(**kw) == B.STATUS[code]
+
+
+def test_frozen_only_call_ignores_dW_pointers():
+    # with final_module_dW = 0, NULL dW/dgain are accepted; the too-small
+    # workspace then fails before any launch
+    assert call(final_module_dW=0, dW=0, dgain=0, workspace_bytes=16) == B.STATUS["SOLO_ERR_WORKSPACE"]
+    assert call(final_module_dW=0, dW=P + 1, dgain=P + 1, workspace_bytes=16) == B.STATUS["SOLO_ERR_WORKSPACE"]
+
+
+def test_workspace_size_boundary():
+    need = B.workspace_size(2, 8, 64, 32, B.SOLO_BF16, True)
+    assert call(workspace_bytes=need - 1) == B.STATUS["SOLO_ERR_WORKSPACE"]

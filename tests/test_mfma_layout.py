@@ -1,0 +1,29 @@
+"""Host check of the matrix-core kernels' LDS chunk layout (mfma_layout.h):
+compiled with g++ from the same header the kernels include, it emulates the
+direct-to-LDS stream and every operand read on the CPU."""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_layout_reads_match_stream(tmp_path):
+    exe = tmp_path / "mfma_layout_check"
+    src = os.path.join(ROOT, "tests", "native", "mfma_layout_check.cpp")
+    inc = os.path.join(ROOT, "paper_2609_35440_amd", "csrc")
+    subprocess.run(["g++", "-std=c++17", "-O1", f"-I{inc}", src, "-o", str(exe)], check=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    print(r.stdout)
+    assert r.returncode == 0, r.stdout
+    rows = {int(m.group(1)): m for m in re.finditer(
+        r"DS=(\d+) padded=(\d) slice=\d+ errors=(\d+) row_conflicts=(\d+) tr_conflicts=(\d+)", r.stdout)}
+    assert sorted(rows) == [32, 64, 96, 128, 160, 192, 224, 256]
+    for ds, m in rows.items():
+        assert int(m.group(3)) == 0, ds
+        if m.group(2) == "1":  # the padded layouts of d = 1024 and 2048 are conflict-free
+            assert int(m.group(4)) == 0 and int(m.group(5)) == 0, ds
