@@ -97,6 +97,20 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
     }
 
 
+def copy_probe(mib: int) -> int:
+    """A plain device-to-device copy of known size: reads and writes mib MiB per launch."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_each_way": n * 4, "launches": 5}), flush=True)
+    return 0
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,7 +122,12 @@ def main(argv=None) -> int:
                     help="tokens per module of the oracle's bounded sample (0 to skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_local_loss_1b.json"),
                     help="HBM traffic of the dominant kernel measured with rocprofv3 counters (JSON), if present")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="instead of the benchmark, run a plain device copy of MIB MiB a few times "
+                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args(argv)
+    if args.copy_probe:
+        return copy_probe(args.copy_probe)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'How the path would "

@@ -71,16 +71,42 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 // lds_base + 16 l.  Issued as inline asm so that the compiler does not track
 // it: the only reader of a chunk is the next step, which starts after an
 // explicit vmcnt(0) wait (wait_vm), and without tracking the compiler adds no
-// conservative waits before unrelated LDS accesses.
+// conservative waits before unrelated LDS accesses.  M0 (the LDS base of the
+// transfer) is a register the compiler reserves, so it is saved and restored;
+// one wait state separates an M0 write from the LDS-DMA that reads it.
 __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, unsigned lds_base, int voffset) {
-    // one wait state between the M0 write and the LDS-DMA read of M0 (gfx9 hazard)
+    unsigned saved;
     asm volatile(
-        "s_mov_b32 m0, %0\n\t"
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
         "s_nop 0\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds"
-        :
+        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
         : "s"(lds_base), "v"(voffset), "s"(rsrc)
-        : "memory", "m0");
+        : "memory");
+}
+
+// All-lane reductions over each 16-lane row of the wave (DPP: quad
+// permutations, then rotations by 4 and 8 inside the row).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max(float x) {
+    x = fmaxf(x, dpp_f<0xB1>(x));   // quad_perm [1,0,3,2]
+    x = fmaxf(x, dpp_f<0x4E>(x));   // quad_perm [2,3,0,1]
+    x = fmaxf(x, dpp_f<0x124>(x));  // row_ror:4
+    x = fmaxf(x, dpp_f<0x128>(x));  // row_ror:8
+    return x;
+}
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x124>(x);
+    x += dpp_f<0x128>(x);
+    return x;
 }
 
 __device__ __forceinline__ unsigned lds_addr(LDS_AS char* p) {
@@ -112,14 +138,14 @@ struct ChunkStream {
 
     // stream rows y0 .. y0 + 15 (this wave's DS columns) of Y into `slice`;
     // rows at or beyond nY read as zeros
-    __device__ __forceinline__ void issue(const bf16* __restrict__ Y, int nY, int d, int y0, LDS_AS char* slice) const {
+    __device__ __forceinline__ void issue(const bf16* __restrict__ Y, int nY, int d, int y0, unsigned slice) const {
+        const int rows = nY - y0;
+        const unsigned rem = rows > 0 ? (unsigned)rows * (unsigned)d * 2u : 0u;
+        const i32x4 rsrc = make_rsrc(Y + (long long)y0 * d, rem);
 #pragma unroll
         for (int q = 0; q < G::NI; ++q) {
-            const int r0 = y0 + layout::stream_row0<DS>(q);
-            const int rows = nY - r0;
-            const unsigned rem = rows > 0 ? (unsigned)rows * (unsigned)d * 2u : 0u;
-            const i32x4 rsrc = make_rsrc(Y + (long long)r0 * d, rem);
-            buffer_load_lds16(rsrc, lds_addr(slice + layout::stream_lds_off<DS>(q)), voff[layout::stream_vidx<DS>(q)]);
+            const int voffset = voff[layout::stream_vidx<DS>(q)] + layout::stream_row0<DS>(q) * d * 2;
+            buffer_load_lds16(rsrc, slice + layout::stream_lds_off<DS>(q), voffset);
         }
     }
 };
@@ -177,7 +203,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     ChunkStream<DS> stream;
     stream.init(d, js, lane);
     // first chunk in flight before the stationary operand is read
-    stream.issue(Y, nY, d, 0, sliceA);
+    const unsigned sliceA_u = lds_addr(sliceA), sliceB_u = lds_addr(sliceB);
+    stream.issue(Y, nY, d, 0, sliceA_u);
     float nx_r = 0.f, nx_lse = 0.f;
     int nx_tgt = -1;
     if (MODE == 1 && yy < nY) {
@@ -217,7 +244,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int c_lo = layout::trread_off<DS>(lane, 0);
     const int c_hi = layout::trread_off<DS>(lane, 1);
 
-    auto step = [&](LDS_AS char* cur, LDS_AS char* nxt, int c) __attribute__((always_inline)) {
+    auto step = [&](LDS_AS char* cur, unsigned nxt, int c) __attribute__((always_inline)) {
         const int y0 = c * YC;
         const float cur_r = nx_r, cur_lse = nx_lse;
         const int cur_tgt = nx_tgt;
@@ -234,12 +261,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
 
         // ---- split-K partial of the logit tile S[y][x] over this wave's columns
+        bf16x8 ay[G::NK];
+#pragma unroll
+        for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
         f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
-            const bf16x8 ay = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
-            S0 = mfma16(ay, xr[0][kk], S0);
-            S1 = mfma16(ay, xr[1][kk], S1);
+            S0 = mfma16(ay[kk], xr[0][kk], S0);
+            S1 = mfma16(ay[kk], xr[1][kk], S1);
         }
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
         *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
@@ -255,11 +284,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (MODE == 0) {
             const bool yok = yg < nY;
             const float z = yok ? sxy * own_r : -INFINITY;
-            float cmax = z;
-            cmax = fmaxf(cmax, __shfl_xor(cmax, 1, 64));
-            cmax = fmaxf(cmax, __shfl_xor(cmax, 2, 64));
-            cmax = fmaxf(cmax, __shfl_xor(cmax, 4, 64));
-            cmax = fmaxf(cmax, __shfl_xor(cmax, 8, 64));
+            const float cmax = row16_max(z);
             float alpha = 1.f;
             if (cmax > m_run + kLazyThresh) {
                 alpha = __expf(m_run - cmax);
@@ -294,22 +319,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     for (int i = 0; i < 16; ++i) acc[b][i] *= al;
             }
         }
+        bf16x4 tlo[G::NB], thi[G::NB];
 #pragma unroll
         for (int b = 0; b < G::NB; ++b) {
-            const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_lo + 64 * b));
-            const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_hi + 64 * b));
-            bf16x8 ay;
-            ay[0] = lo[0]; ay[1] = lo[1]; ay[2] = lo[2]; ay[3] = lo[3];
-            ay[4] = hi[0]; ay[5] = hi[1]; ay[6] = hi[2]; ay[7] = hi[3];
-            acc[b] = mfma32(ay, gfrag, acc[b]);
+            tlo[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_lo + 64 * b));
+            thi[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_hi + 64 * b));
+        }
+#pragma unroll
+        for (int b = 0; b < G::NB; ++b) {
+            bf16x8 at;
+            at[0] = tlo[b][0]; at[1] = tlo[b][1]; at[2] = tlo[b][2]; at[3] = tlo[b][3];
+            at[4] = thi[b][0]; at[5] = thi[b][1]; at[6] = thi[b][2]; at[7] = thi[b][3];
+            acc[b] = mfma32(at, gfrag, acc[b]);
         }
         wait_vm();
     };
 
     wait_vm();
     for (int c = 0; c < nchunks; c += 2) {
-        step(sliceA, sliceB, c);
-        if (c + 1 < nchunks) step(sliceB, sliceA, c + 1);
+        step(sliceA, sliceB_u, c);
+        if (c + 1 < nchunks) step(sliceB, sliceA_u, c + 1);
     }
 
     // ---- epilogues.  acc[b] lane layout: x = lane%32,
@@ -319,8 +348,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     if (MODE == 0) {
         // finish the online softmax of rows 4w..4w+3
         float s = s_part, zy = zy_part;
-        s += __shfl_xor(s, 1, 64); s += __shfl_xor(s, 2, 64); s += __shfl_xor(s, 4, 64); s += __shfl_xor(s, 8, 64);
-        zy += __shfl_xor(zy, 1, 64); zy += __shfl_xor(zy, 2, 64); zy += __shfl_xor(zy, 4, 64); zy += __shfl_xor(zy, 8, 64);
+        s = row16_sum(s);
+        zy = row16_sum(zy);
         if (yy == 0) {
             const float lse = m_run + logf(s);
             const bool tok = own_tgt >= 0 && own_tgt < nY;

@@ -3,7 +3,7 @@
 #include <cmath>
 #include <cstdint>
 
-#include "../../include/solo_readout.h"
+#include "solo_readout.h"
 #include "solo_internal.h"
 
 namespace {
