@@ -97,6 +97,17 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
     }
 
 
+def kernel_sources_hash() -> str:
+    """Hash of the matrix-core kernel sources (stamps counter-derived traffic)."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in ("k_mfma.hip", "mfma_layout.h", "solo_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def copy_probe(mib: int) -> int:
     """A plain device-to-device copy of known size: reads and writes mib MiB per launch."""
     import torch
@@ -118,7 +129,7 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="1b", help="workload shape (solo_inputs.CONFIGS key)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-sample-tokens", type=int, default=2048,
+    ap.add_argument("--cpu-sample-tokens", type=int, default=8192,
                     help="tokens per module of the oracle's bounded sample (0 to skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_local_loss_1b.json"),
                     help="HBM traffic of the dominant kernel measured with rocprofv3 counters (JSON), if present")
@@ -215,7 +226,9 @@ def main(argv=None) -> int:
         try:
             with open(args.traffic) as f:
                 tr = json.load(f)
-            if tr.get("config") == args.config and tr.get("family") == family:
+            # counters count only for the kernel source they were taken on
+            if (tr.get("config") == args.config and tr.get("family") == family
+                    and tr.get("kernel_sources_sha256_16") == kernel_sources_hash()):
                 traffic = tr.get("bytes_per_launch")
         except Exception:
             traffic = None

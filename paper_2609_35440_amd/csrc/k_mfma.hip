@@ -154,7 +154,13 @@ struct ChunkStream {
 // in-flight chunk prefetch.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// vmcnt(0) (expcnt and lgkmcnt not waited for: gfx9 encoding 0x0F70) through
+// the builtin, so that the compiler's own wait tracking sees it too, followed
+// by a compiler barrier that keeps LDS reads of the new chunk below it.
+__device__ __forceinline__ void wait_vm() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    asm volatile("" ::: "memory");
+}
 
 // MODE 0: local-loss pass, grid (ceil(T/32), K).
 // MODE 1: readout-gradient pass of module K-1, grid (ceil(V/32)).
@@ -170,6 +176,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     __shared__ float abuf[XR];
     __shared__ float sbuf[XR];
     __shared__ float cbuf[NW * XR];
+    __shared__ __attribute__((aligned(16))) float recA[YC * 4];  // readout-gradient pass: per-token records
+    __shared__ __attribute__((aligned(16))) float recB[YC * 4];
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -205,13 +213,18 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     // first chunk in flight before the stationary operand is read
     const unsigned sliceA_u = lds_addr(sliceA), sliceB_u = lds_addr(sliceB);
     stream.issue(Y, nY, d, 0, sliceA_u);
-    float nx_r = 0.f, nx_lse = 0.f;
-    int nx_tgt = -1;
-    if (MODE == 1 && yy < nY) {
-        nx_r = a.rstd[modoff + yy];
-        nx_lse = a.lse[modoff + yy];
-        nx_tgt = a.targets[modoff + yy];
-    }
+    // readout-gradient pass: the 16 per-token records {lse, rstd, target, 0}
+    // of a chunk stream into recA / recB next to the chunk itself
+    const unsigned recA_u = lds_addr((LDS_AS char*)(LDS_AS void*)recA);
+    const unsigned recB_u = lds_addr((LDS_AS char*)(LDS_AS void*)recB);
+    auto issue_rec = [&](int y0, unsigned dst) __attribute__((always_inline)) {
+        if (MODE == 1 && w == 0 && lane < YC) {
+            const int rows = nY - y0;
+            const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
+            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (long long)y0, rem), dst, lane * 16);
+        }
+    };
+    issue_rec(0, recA_u);
 
     // stationary operand: B of the 16x16x32 logit product, lane holds
     // X[x0 + 16 xb + lane%16][js + 32 kk + 8 (lane/16) .. +7]
@@ -244,20 +257,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int c_lo = layout::trread_off<DS>(lane, 0);
     const int c_hi = layout::trread_off<DS>(lane, 1);
 
-    auto step = [&](LDS_AS char* cur, unsigned nxt, int c) __attribute__((always_inline)) {
+    auto step = [&](LDS_AS char* cur, unsigned nxt, LDS_AS float* rec, unsigned rec_nxt, int c)
+                    __attribute__((always_inline)) {
         const int y0 = c * YC;
-        const float cur_r = nx_r, cur_lse = nx_lse;
-        const int cur_tgt = nx_tgt;
         if (c + 1 < nchunks) {
             stream.issue(Y, nY, d, y0 + YC, nxt);
-            if (MODE == 1) {
-                const int yn = y0 + YC + yy;
-                if (yn < nY) {
-                    nx_r = a.rstd[modoff + yn];
-                    nx_lse = a.lse[modoff + yn];
-                    nx_tgt = a.targets[modoff + yn];
-                }
-            }
+            issue_rec(y0 + YC, rec_nxt);
         }
 
         // ---- split-K partial of the logit tile S[y][x] over this wave's columns
@@ -300,9 +305,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const int xg = x0 + xo;
             gval = 0.f;
             if (yg < nY && xg < nX) {
-                const float z = sxy * cur_r;
-                const float p = __expf(z - cur_lse);
-                gval = (p - (cur_tgt == xg ? 1.f : 0.f)) * cur_r * a.inv_T;
+                const f32x4 r4 = *(LDS_AS f32x4*)(rec + 4 * yy);   // {lse, rstd, target, 0}
+                const float z = sxy * r4[1];
+                const float p = __expf(z - r4[0]);
+                gval = (p - (__float_as_int(r4[2]) == xg ? 1.f : 0.f)) * r4[1] * a.inv_T;
             }
         }
         gbuf[xo * YC + yy] = (bf16)gval;
@@ -332,13 +338,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             at[4] = thi[b][0]; at[5] = thi[b][1]; at[6] = thi[b][2]; at[7] = thi[b][3];
             acc[b] = mfma32(at, gfrag, acc[b]);
         }
+        __builtin_amdgcn_sched_barrier(0);
         wait_vm();
     };
 
     wait_vm();
     for (int c = 0; c < nchunks; c += 2) {
-        step(sliceA, sliceB_u, c);
-        if (c + 1 < nchunks) step(sliceB, sliceA_u, c + 1);
+        step(sliceA, sliceB_u, (LDS_AS float*)(LDS_AS void*)recA, recB_u, c);
+        if (c + 1 < nchunks) step(sliceB, sliceA_u, (LDS_AS float*)(LDS_AS void*)recB, recA_u, c + 1);
     }
 
     // ---- epilogues.  acc[b] lane layout: x = lane%32,
@@ -357,6 +364,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (x0 + xo < nX) {
                 a.lse[modoff + x0 + xo] = lse;
                 a.rowloss[modoff + x0 + xo] = rl;
+                if (a.rowrec && k == a.K - 1) {
+                    f32x4 rec4 = {lse, own_r, __int_as_float(own_tgt), 0.f};
+                    *(f32x4*)(a.rowrec + 4 * (long long)(x0 + xo)) = rec4;
+                }
             }
             sbuf[xo] = 1.f / s;
         }

@@ -63,13 +63,23 @@ __global__ void k_module_loss(const float* __restrict__ rowloss, float* __restri
     if (threadIdx.x == 0) losses[k] = (float)(red[0] / (double)T);
 }
 
-// dgain[j] = sum over vocabulary tiles of part[tile][j], fixed order.
+// dgain[j] = sum over vocabulary tiles of part[tile][j], fixed order: a
+// block of 256 threads covers 32 columns; its 8 thread groups sum every
+// eighth tile, then the 8 group sums are added in group order.
 __global__ void k_dgain_reduce(const float* __restrict__ part, float* __restrict__ dgain, int ntiles, int d) {
-    int j = blockIdx.x * blockDim.x + threadIdx.x;
-    if (j >= d) return;
+    __shared__ double red[8][32];
+    const int jl = threadIdx.x & 31, grp = threadIdx.x >> 5;
+    const int j = blockIdx.x * 32 + jl;
     double acc = 0.0;
-    for (int i = 0; i < ntiles; ++i) acc += (double)part[(long long)i * d + j];
-    dgain[j] = (float)acc;
+    if (j < d)
+        for (int i = grp; i < ntiles; i += 8) acc += (double)part[(long long)i * d + j];
+    red[grp][jl] = acc;
+    __syncthreads();
+    if (grp == 0 && j < d) {
+        double s = 0.0;
+        for (int g = 0; g < 8; ++g) s += red[g][jl];
+        dgain[j] = (float)s;
+    }
 }
 
 }  // namespace
@@ -102,7 +112,7 @@ hipError_t launch_module_loss(const float* rowloss, float* losses, int K, int T,
 }
 
 hipError_t launch_dgain_reduce(const float* part, float* dgain, int ntiles, int d, hipStream_t s) {
-    hipLaunchKernelGGL(k_dgain_reduce, dim3((d + 255) / 256), dim3(256), 0, s, part, dgain, ntiles, d);
+    hipLaunchKernelGGL(k_dgain_reduce, dim3((d + 31) / 32), dim3(256), 0, s, part, dgain, ntiles, d);
     return hipGetLastError();
 }
 

@@ -13,7 +13,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-    size_t wg, rstd, lse, rowloss, dgp, total;
+    size_t wg, rstd, lse, rowloss, rowrec, dgp, total;
     int ntiles;
     bool mfma;
 };
@@ -41,6 +41,8 @@ bool make_layout(int K, int T, int d, int V, int dtype, int fdw, Layout* L) {
     off = align_up(off + (size_t)K * T * 4);
     L->rowloss = off;
     off = align_up(off + (size_t)K * T * 4);
+    L->rowrec = off;
+    off = align_up(off + (fdw ? (size_t)T * 16 : 0));
     L->ntiles = fdw ? (V + vtile - 1) / vtile : 0;
     L->dgp = off;
     off = align_up(off + (size_t)L->ntiles * d * 4);
@@ -125,6 +127,7 @@ int solo_readout_fwd_bwd_profiled(int K, int T, int d, int V, int dtype, float e
     a.rstd = (const float*)(ws + L.rstd);
     a.lse = (float*)(ws + L.lse);
     a.rowloss = row_loss ? row_loss : (float*)(ws + L.rowloss);
+    a.rowrec = final_module_dW ? (float*)(ws + L.rowrec) : nullptr;
     a.dh = dh;
     a.dW = final_module_dW ? dW : nullptr;
     a.dgain_part = (float*)(ws + L.dgp);

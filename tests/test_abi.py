@@ -45,18 +45,19 @@ def test_status_strings():
 
 
 def test_workspace_has_no_TV_term():
-    # bf16 matrix-core family: Wg (V d 2) + rstd, lse, row_loss (3 K T 4) + dgain partials (ceil(V/32) d 4)
+    # bf16 matrix-core family: Wg (V d 2) + rstd, lse, row_loss (3 K T 4) + final-module token
+    # records (T 16) + dgain partials (ceil(V/32) d 4)
     def al(x):
         return (x + 255) // 256 * 256
 
     for K, T, d, V in [(4, 16384, 2048, 32000), (2, 32768, 2048, 128256), (4, 8192, 1024, 32000), (1, 1, 256, 1)]:
-        want = al(V * d * 2) + 3 * al(K * T * 4) + al(-(-V // 32) * d * 4)
+        want = al(V * d * 2) + 3 * al(K * T * 4) + al(T * 16) + al(-(-V // 32) * d * 4)
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, True) == want
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == al(V * d * 2) + 3 * al(K * T * 4)
-    # doubling T with V fixed grows the workspace by K*T*12 bytes only
+    # doubling T with V fixed grows the workspace by K*T*12 + T*16 bytes only
     a = B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True)
     b = B.workspace_size(4, 32768, 2048, 32000, B.SOLO_BF16, True)
-    assert b - a == 3 * 4 * 16384 * 4
+    assert b - a == 3 * 4 * 16384 * 4 + 16384 * 16
     # far below one module's T x V fp32 logits (2.1 GB at the 1B shape)
     assert a < 16384 * 32000 * 4 / 4
     # invalid arguments -> 0
