@@ -24,26 +24,19 @@
 // stationary operand stay in registers for the whole pass; the streamed
 // chunk goes HBM/L2 -> LDS directly and is read twice from LDS: row-wise for
 // the logit product and with the transposing read for the second product.
-#include "mfma_layout.h"
-#include "solo_internal.h"
+#include "mfma_common.h"
 
 namespace solo {
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
-#define LDS_AS __attribute__((address_space(3)))
+using namespace mfma;
 
 constexpr int NW = layout::NW;  // waves per workgroup
 constexpr int NTHR = NW * 64;
 constexpr int XR = kMfmaRows;  // stationary rows per workgroup (32)
 constexpr int YC = layout::YC;  // streamed rows per chunk
 constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: conflict-free 16 B writes
-constexpr float kLazyThresh = 8.0f;  // re-base the running max only when it grows by more than this
 
 template <int DS>
 struct Geo : layout::Geo<DS> {
@@ -54,119 +47,13 @@ struct Geo : layout::Geo<DS> {
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
-__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ __forceinline__ float bf16_bits_to_f32(unsigned short u) {
-    return __uint_as_float(((unsigned)u) << 16);
-}
-
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-
-// Direct buffer -> LDS load of 16 bytes per lane; lane l's bytes land at
-// lds_base + 16 l.  Issued as inline asm so that the compiler does not track
-// it: the only reader of a chunk is the next step, which starts after an
-// explicit vmcnt(0) wait (wait_vm), and without tracking the compiler adds no
-// conservative waits before unrelated LDS accesses.  M0 (the LDS base of the
-// transfer) is a register the compiler reserves, so it is saved and restored;
-// one wait state separates an M0 write from the LDS-DMA that reads it.
-__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, unsigned lds_base, int voffset) {
-    unsigned saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-        "s_nop 0\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds_base), "v"(voffset), "s"(rsrc)
-        : "memory");
-}
-
-// All-lane reductions over each 16-lane row of the wave (DPP: quad
-// permutations, then rotations by 4 and 8 inside the row).
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float x) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float row16_max(float x) {
-    x = fmaxf(x, dpp_f<0xB1>(x));   // quad_perm [1,0,3,2]
-    x = fmaxf(x, dpp_f<0x4E>(x));   // quad_perm [2,3,0,1]
-    x = fmaxf(x, dpp_f<0x124>(x));  // row_ror:4
-    x = fmaxf(x, dpp_f<0x128>(x));  // row_ror:8
-    return x;
-}
-__device__ __forceinline__ float row16_sum(float x) {
-    x += dpp_f<0xB1>(x);
-    x += dpp_f<0x4E>(x);
-    x += dpp_f<0x124>(x);
-    x += dpp_f<0x128>(x);
-    return x;
-}
-
-__device__ __forceinline__ unsigned lds_addr(LDS_AS char* p) {
-    return __builtin_amdgcn_readfirstlane((unsigned)(unsigned long long)p);
-}
-
-// Buffer resource over [base, base + bytes): loads at or beyond `bytes`
-// return zeros, which pads the ragged last chunk.
-__device__ __forceinline__ i32x4 make_rsrc(const void* base, unsigned bytes) {
-    const unsigned long long a = (unsigned long long)base;
-    i32x4 r;
-    r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)a);
-    r[1] = __builtin_amdgcn_readfirstlane((int)(unsigned)(a >> 32));
-    r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
-    r[3] = 0x00020000;
-    return r;
-}
-
-// The direct-to-LDS stream of one chunk (layout in mfma_layout.h).
-template <int DS>
-struct ChunkStream {
-    using G = layout::Geo<DS>;
-    int voff[G::NV];
-
-    __device__ __forceinline__ void init(int d, int js, int lane) {
-#pragma unroll
-        for (int v = 0; v < G::NV; ++v) voff[v] = layout::stream_voff<DS>(v, d, js, lane);
-    }
-
-    // stream rows y0 .. y0 + 15 (this wave's DS columns) of Y into `slice`;
-    // rows at or beyond nY read as zeros
-    __device__ __forceinline__ void issue(const bf16* __restrict__ Y, int nY, int d, int y0, unsigned slice) const {
-        const int rows = nY - y0;
-        const unsigned rem = rows > 0 ? (unsigned)rows * (unsigned)d * 2u : 0u;
-        const i32x4 rsrc = make_rsrc(Y + (long long)y0 * d, rem);
-#pragma unroll
-        for (int q = 0; q < G::NI; ++q) {
-            const int voffset = voff[layout::stream_vidx<DS>(q)] + layout::stream_row0<DS>(q) * d * 2;
-            buffer_load_lds16(rsrc, slice + layout::stream_lds_off<DS>(q), voffset);
-        }
-    }
-};
-
-// Barrier for LDS traffic only: unlike __syncthreads it does not drain the
-// in-flight chunk prefetch.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// vmcnt(0) (expcnt and lgkmcnt not waited for: gfx9 encoding 0x0F70) through
-// the builtin, so that the compiler's own wait tracking sees it too, followed
-// by a compiler barrier that keeps LDS reads of the new chunk below it.
-__device__ __forceinline__ void wait_vm() {
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    asm volatile("" ::: "memory");
-}
-
 // MODE 0: local-loss pass, grid (ceil(T/32), K).
 // MODE 1: readout-gradient pass of module K-1, grid (ceil(V/32)).
 template <int MODE, int DS>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     using G = Geo<DS>;
+    // the stream of a chunk is issued in batches [0, kDma1), [kDma1, kDma2), [kDma2, NI)
+    constexpr int kDma1 = (3 * G::NI + 7) / 8, kDma2 = (6 * G::NI + 7) / 8;
     // Separate LDS objects, so that the compiler can tell the chunk being read
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
@@ -207,6 +94,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         own_r = a.rstd[modoff + x0 + xo];
         own_tgt = a.targets[modoff + x0 + xo];
     }
+    const float own_r2 = own_r * kLog2e;
 
     ChunkStream<DS> stream;
     stream.init(d, js, lane);
@@ -249,7 +137,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[b][i] = 0.f;
 
-    // online softmax state (MODE 0), per lane: row xo, streamed column yy
+    // online softmax state (MODE 0, base 2), per lane: row xo, streamed column yy
     float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
 
     // per-lane parts of the LDS addresses; the unrolled loops add 64 * kk or 64 * b
@@ -260,58 +148,69 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     auto step = [&](LDS_AS char* cur, unsigned nxt, LDS_AS float* rec, unsigned rec_nxt, int c)
                     __attribute__((always_inline)) {
         const int y0 = c * YC;
-        if (c + 1 < nchunks) {
-            stream.issue(Y, nY, d, y0 + YC, nxt);
-            issue_rec(y0 + YC, rec_nxt);
-        }
+        const bool more = c + 1 < nchunks;
+        const i32x4 nrs = ChunkStream<DS>::rsrc(Y, nY, d, y0 + YC);
 
-        // ---- split-K partial of the logit tile S[y][x] over this wave's columns
+        // ---- split-K partial of the logit tile S[y][x] over this wave's columns.
+        // All operand reads go out first, ahead of the data of the next chunk,
+        // whose stream is issued in three batches (here, after these products
+        // and after the elementwise step) so that neither the texture unit's
+        // queue nor the LDS write port sees the whole chunk at once.
         bf16x8 ay[G::NK];
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
+        if (more) {
+            stream.template issue_range<0, kDma1>(nrs, d, nxt);
+            issue_rec(y0 + YC, rec_nxt);
+        }
         f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
             S0 = mfma16(ay[kk], xr[0][kk], S0);
             S1 = mfma16(ay[kk], xr[1][kk], S1);
         }
+        if (more) stream.template issue_range<kDma1, kDma2>(nrs, d, nxt);
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
         *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
         *(f32x4*)(part + (w * XR + 16 + (lane & 15)) * PP + 4 * (lane >> 4)) = S1;
         lds_barrier();
 
         // ---- elementwise step for rows xo = 4w .. 4w+3 (lane: row xo, column yy)
-        float sxy = 0.f;
+        float q[NW];
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) sxy += part[(ww * XR + xo) * PP + yy];
+        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + yy];
+        static_assert(NW == 8, "partial-sum tree");
+        const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
         const int yg = y0 + yy;
         float gval;
         if (MODE == 0) {
-            const bool yok = yg < nY;
-            const float z = yok ? sxy * own_r : -INFINITY;
-            const float cmax = row16_max(z);
+            // columns past the end of the vocabulary get z = -inf (an additive
+            // mask rather than a branch, so the partial reads stay unconditional)
+            const float ymask = (yg < nY) ? 0.f : -INFINITY;
+            const float zc = __builtin_fmaf(sxy, own_r2, ymask);
             float alpha = 1.f;
-            if (cmax > m_run + kLazyThresh) {
-                alpha = __expf(m_run - cmax);
-                s_part *= alpha;
-                m_run = cmax;
+            if (__builtin_expect(__any(zc > m_run + kLazyThresh2), 0)) {  // wave-uniform
+                const float cmax = row16_max(zc);
+                if (cmax > m_run + kLazyThresh2) {
+                    alpha = __builtin_amdgcn_exp2f(m_run - cmax);
+                    s_part *= alpha;
+                    m_run = cmax;
+                }
             }
-            const float p = yok ? __expf(z - m_run) : 0.f;
+            const float p = __builtin_amdgcn_exp2f(zc - m_run);
             s_part += p;
-            if (yg == own_tgt) zy_part = z;
+            if (yg == own_tgt) zy_part = zc;
             gval = p;
-            if (yy == 0) abuf[xo] = alpha;
+            abuf[xo] = alpha;  // the 16 lanes of a row store the same value
         } else {
-            const int xg = x0 + xo;
-            gval = 0.f;
-            if (yg < nY && xg < nX) {
-                const f32x4 r4 = *(LDS_AS f32x4*)(rec + 4 * yy);   // {lse, rstd, target, 0}
-                const float z = sxy * r4[1];
-                const float p = __expf(z - r4[0]);
-                gval = (p - (__float_as_int(r4[2]) == xg ? 1.f : 0.f)) * r4[1] * a.inv_T;
-            }
+            // record {lse log2 e, r log2 e, target, r / T}; rows past the end
+            // read as zeros and give gval = 0
+            const f32x4 r4 = *(LDS_AS f32x4*)(rec + 4 * yy);
+            const float p = __builtin_amdgcn_exp2f(sxy * r4[1] - r4[0]);
+            gval = (p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f)) * r4[3];
         }
         gbuf[xo * YC + yy] = (bf16)gval;
+        if (more) stream.template issue_range<kDma2, G::NI>(nrs, d, nxt);
         lds_barrier();
 
         // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
@@ -358,14 +257,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         s = row16_sum(s);
         zy = row16_sum(zy);
         if (yy == 0) {
-            const float lse = m_run + logf(s);
+            const float lse2 = m_run + __log2f(s);
             const bool tok = own_tgt >= 0 && own_tgt < nY;
-            const float rl = tok ? lse - zy : __int_as_float(0x7fc00000);
+            const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
             if (x0 + xo < nX) {
-                a.lse[modoff + x0 + xo] = lse;
+                a.lse[modoff + x0 + xo] = lse2 * kLn2;
                 a.rowloss[modoff + x0 + xo] = rl;
                 if (a.rowrec && k == a.K - 1) {
-                    f32x4 rec4 = {lse, own_r, __int_as_float(own_tgt), 0.f};
+                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), own_r * a.inv_T};
                     *(f32x4*)(a.rowrec + 4 * (long long)(x0 + xo)) = rec4;
                 }
             }

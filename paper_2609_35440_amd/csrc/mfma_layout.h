@@ -15,26 +15,28 @@
 namespace solo {
 namespace layout {
 
-constexpr int NW = 8;   // waves per workgroup; wave w owns columns [w DS, (w + 1) DS)
+constexpr int NW = 8;   // waves per workgroup of the two-waves-per-SIMD kernels
 constexpr int YC = 16;  // streamed rows per chunk
 
 template <int DS>
 struct Geo {
+    // wave w owns columns [w DS, (w + 1) DS) of the streamed rows
     static constexpr int GPR = DS / 8;                      // 16-byte granules per row of a wave slice
     static constexpr int NI = DS / 32;                      // 1 KiB direct-to-LDS instructions per slice
-    static constexpr bool PADDED = (NI % 4) == 0;           // padded layout (DS = 128, 256)
+    // padded layout (DS = 128, 256, 512): every 1 KiB instruction covers whole rows
+    static constexpr bool PADDED = (NI % 4) == 0 && (512 % DS) == 0;
     static constexpr int IPITCH = PADDED ? 1088 : 1024;     // bytes between the instructions' destinations
     static constexpr int SLICE = (NI - 1) * IPITCH + 1024;  // bytes of one wave's chunk slice
     static constexpr int NV = PADDED ? NI / 4 : NI;         // distinct per-lane stream offsets
-    static_assert(DS % 32 == 0 && DS >= 32 && DS <= 256, "slice width");
+    static_assert(DS % 32 == 0 && DS >= 32 && DS <= 512, "slice width");
 };
 
 // Byte offset of 16-byte granule g (columns 8 g .. 8 g + 7 of the slice) of
 // streamed row r (0..15) inside a wave's chunk slice.
 //
 // Padded layout: instruction q of the direct-to-LDS stream writes rows
-// q, q + NI, ... back to back at q * 1088 (so its rows start at byte 64 q mod
-// 256); inside a row, the low two bits of the granule index are XORed with
+// q, q + NI, ... (one row if DS = 512) back to back at q * 1088 (so its rows
+// start at byte 64 q mod 256); inside a row, the low two bits of the granule index are XORed with
 // (r >> 2) & 3.  Row r then starts at bank slot 4 (r & 3) (of 16 slots of 16
 // bytes) and both read patterns are conflict-free: the row-wise reads (16 rows
 // at one granule) and the transposing reads (4 rows x 4 granules).  The offset

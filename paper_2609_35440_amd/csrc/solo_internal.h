@@ -23,7 +23,7 @@ struct FusedArgs {
     const int32_t* targets;  // [K][T]
     const float* rstd;    // [K][T] 1/sqrt(mean h^2 + eps)
     float* lse;           // [K][T] log-sum-exp (written by the local-loss pass)
-    float* rowrec;        // [T][4] final module: {lse, rstd, target bits, 0} per token (16-byte records)
+    float* rowrec;        // [T][4] final module: {lse log2 e, rstd log2 e, target bits, rstd / T} per token
     float* rowloss;       // [K][T] per-token cross-entropy
     void* dh;             // [K][T][d] elem
     float* dW;            // [V][d]

@@ -16,13 +16,14 @@
 
 using namespace solo::layout;
 
-template <int DS>
+// NWAVES waves of DS columns each cover the row width d = NWAVES DS.
+template <int DS, int NWAVES>
 int check(int& conflicts_row, int& conflicts_tr) {
     using G = Geo<DS>;
-    const int d = DS * NW;
+    const int d = DS * NWAVES;
     int errors = 0;
     conflicts_row = conflicts_tr = 0;
-    for (int w = 0; w < NW; ++w) {
+    for (int w = 0; w < NWAVES; ++w) {
         const int js = w * DS;
         // LDS byte -> (row, column) of the bf16 element stored there
         std::map<int, std::pair<int, int>> lds;
@@ -84,12 +85,12 @@ int check(int& conflicts_row, int& conflicts_tr) {
     return errors;
 }
 
-template <int DS>
+template <int DS, int NWAVES = NW>
 int report() {
     int cr = 0, ct = 0;
-    const int e = check<DS>(cr, ct);
-    std::printf("DS=%d padded=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d\n", DS, (int)Geo<DS>::PADDED,
-                Geo<DS>::SLICE, e, cr, ct);
+    const int e = check<DS, NWAVES>(cr, ct);
+    std::printf("DS=%d waves=%d padded=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d\n", DS, NWAVES,
+                (int)Geo<DS>::PADDED, Geo<DS>::SLICE, e, cr, ct);
     return e;
 }
 
@@ -103,5 +104,9 @@ int main() {
     e += report<192>();
     e += report<224>();
     e += report<256>();
+    // one-wave-per-SIMD kernels: 4 waves of d / 4 columns
+    e += report<256, 4>();
+    e += report<384, 4>();
+    e += report<512, 4>();
     return e == 0 ? 0 : 1;
 }

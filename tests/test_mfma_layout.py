@@ -20,10 +20,11 @@ def test_layout_reads_match_stream(tmp_path):
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     print(r.stdout)
     assert r.returncode == 0, r.stdout
-    rows = {int(m.group(1)): m for m in re.finditer(
-        r"DS=(\d+) padded=(\d) slice=\d+ errors=(\d+) row_conflicts=(\d+) tr_conflicts=(\d+)", r.stdout)}
-    assert sorted(rows) == [32, 64, 96, 128, 160, 192, 224, 256]
-    for ds, m in rows.items():
-        assert int(m.group(3)) == 0, ds
-        if m.group(2) == "1":  # the padded layouts of d = 1024 and 2048 are conflict-free
-            assert int(m.group(4)) == 0 and int(m.group(5)) == 0, ds
+    rows = {(int(m.group(1)), int(m.group(2))): m for m in re.finditer(
+        r"DS=(\d+) waves=(\d+) padded=(\d) slice=\d+ errors=(\d+) row_conflicts=(\d+) tr_conflicts=(\d+)", r.stdout)}
+    assert sorted(rows) == [(32, 8), (64, 8), (96, 8), (128, 8), (160, 8), (192, 8), (224, 8), (256, 4), (256, 8),
+                            (384, 4), (512, 4)]
+    for key, m in rows.items():
+        assert int(m.group(4)) == 0, key
+        if m.group(3) == "1":  # the padded layouts (DS = 128, 256, 512) are conflict-free
+            assert int(m.group(5)) == 0 and int(m.group(6)) == 0, key
