@@ -102,7 +102,7 @@ def kernel_sources_hash() -> str:
     import hashlib
 
     h = hashlib.sha256()
-    for f in ("k_mfma.hip", "mfma_layout.h", "solo_internal.h"):
+    for f in ("k_mfma.hip", "mfma_common.h", "mfma_layout.h", "solo_internal.h"):
         with open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -2,10 +2,13 @@
 // direct-to-LDS stream of one chunk slice with the functions of
 // mfma_layout.h, then every row-wise and transposing operand read, and check
 // that each returns the element its MFMA operand needs.  Also counts LDS bank
-// conflicts (64 banks of 4 bytes) of both read patterns.
+// conflicts of both read patterns with the service model measured on gfx950:
+// a 16-byte-per-lane read is served 8 lanes at a time over 32 banks of 4
+// bytes, the 8-byte transposing read 32 lanes at a time over 64 banks.
 // Transposing read semantics (ds_read_b64_tr_b16, per 16-lane group): lane i
 // receives, as element y, the 16-bit value (i % 4) of the 8 bytes addressed by
 // lane 4 y + i / 4 of its group.
+#include <algorithm>
 #include <cstdio>
 #include <map>
 #include <set>
@@ -15,6 +18,21 @@
 #include "mfma_layout.h"
 
 using namespace solo::layout;
+
+// Extra service passes caused by bank conflicts: lanes are served in groups
+// of `pass` lanes; within a group, a bank holding k distinct dwords costs k - 1.
+static int conflicts(const int* addr, int width, int pass, int nbanks) {
+    int extra = 0;
+    for (int p = 0; p < 64; p += pass) {
+        std::map<int, std::set<int>> banks;
+        for (int l = p; l < p + pass; ++l)
+            for (int wd = 0; wd < width / 4; ++wd) banks[(addr[l] / 4 + wd) % nbanks].insert(addr[l] / 4 + wd);
+        int worst = 1;
+        for (auto& b : banks) worst = std::max(worst, (int)b.second.size());
+        extra += worst - 1;
+    }
+    return extra;
+}
 
 // NWAVES waves of DS columns each cover the row width d = NWAVES DS.
 template <int DS, int NWAVES>
@@ -42,19 +60,17 @@ int check(int& conflicts_row, int& conflicts_tr) {
         if ((int)lds.size() != 16 * DS) ++errors;  // every element of the 16 x DS slice exactly once
         // row-wise reads: lane -> row lane % 16, columns js + 32 kk + 8 (lane / 16) + e
         for (int kk = 0; kk < DS / 32; ++kk) {
-            for (int g16 = 0; g16 < 4; ++g16) {
-                std::set<int> slots;
-                for (int l = 16 * g16; l < 16 * g16 + 16; ++l) {
-                    const int base = rowread_off<DS>(l) + 64 * kk;
-                    slots.insert((base / 16) % 16);
-                    for (int e = 0; e < 8; ++e) {
-                        auto it = lds.find(base + 2 * e);
-                        std::pair<int, int> want{l & 15, js + 32 * kk + 8 * (l >> 4) + e};
-                        if (it == lds.end() || it->second != want) ++errors;
-                    }
+            int addr[64];
+            for (int l = 0; l < 64; ++l) {
+                const int base = rowread_off<DS>(l) + 64 * kk;
+                addr[l] = base;
+                for (int e = 0; e < 8; ++e) {
+                    auto it = lds.find(base + 2 * e);
+                    std::pair<int, int> want{l & 15, js + 32 * kk + 8 * (l >> 4) + e};
+                    if (it == lds.end() || it->second != want) ++errors;
                 }
-                conflicts_row += 16 - (int)slots.size();
             }
+            conflicts_row += conflicts(addr, 16, 8, 32);
         }
         // transposing reads of block b: lane -> m = column js + 32 b + lane % 32,
         // k = rows 8 (lane / 32) + 4 half + y
@@ -62,14 +78,7 @@ int check(int& conflicts_row, int& conflicts_tr) {
             for (int half = 0; half < 2; ++half) {
                 int addr[64];
                 for (int l = 0; l < 64; ++l) addr[l] = trread_off<DS>(l, half) + 64 * b;
-                for (int h32 = 0; h32 < 2; ++h32) {
-                    std::set<int> banks;
-                    for (int l = 32 * h32; l < 32 * h32 + 32; ++l) {
-                        banks.insert((addr[l] / 4) % 64);
-                        banks.insert((addr[l] / 4 + 1) % 64);
-                    }
-                    conflicts_tr += 64 - (int)banks.size();
-                }
+                conflicts_tr += conflicts(addr, 8, 32, 64);
                 for (int l = 0; l < 64; ++l) {
                     const int grp = l / 16, i = l % 16;
                     for (int y = 0; y < 4; ++y) {
