@@ -39,6 +39,7 @@ def _hip():
     lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
     lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    lib.hipMemGetInfo.argtypes = [ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
     return lib
 
 
@@ -197,6 +198,18 @@ def main(argv=None) -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # device memory: torch's allocator peak over one call (the library itself
+    # allocates nothing), and the driver's free-memory reading around it
+    free0 = ctypes.c_size_t(0)
+    total = ctypes.c_size_t(0)
+    assert hip.hipMemGetInfo(ctypes.byref(free0), ctypes.byref(total)) == 0
+    base_alloc = torch.cuda.memory_allocated(dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    step()
+    torch.cuda.synchronize()
+    peak_delta = torch.cuda.max_memory_allocated(dev) - base_alloc
+    free1 = ctypes.c_size_t(0)
+    assert hip.hipMemGetInfo(ctypes.byref(free1), ctypes.byref(total)) == 0
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(events[i])
@@ -253,6 +266,11 @@ def main(argv=None) -> int:
         "module_tokens_per_s": K * tokens_per_s,
         "stage_ms": stage_ms,
         "event_ms_per_step": float(np.median(step_ms)),
+        "event_ms_per_step_min": float(np.min(step_ms)),
+        "workspace_bytes": int(ws.numel()),
+        "peak_alloc_delta_bytes": int(peak_delta),
+        "driver_free_delta_bytes": int(free0.value) - int(free1.value),
+        "one_module_tv_bf16_bytes": int(T) * int(V) * 2,
         "roofline": {
             "bound": "mfma",
             "kernel": "local-loss pass (logits + online log-sum-exp + dh), all K modules",
@@ -261,6 +279,7 @@ def main(argv=None) -> int:
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": traffic,
+            "hbm_gb_per_s": (traffic / (ll_ms / 1e3) / 1e9) if traffic else None,
             "algorithmic_flops_per_launch": ll_flops,
             "launch_ms": ll_ms,
         },

@@ -11,3 +11,5 @@ from .solo_oracle import (  # noqa: F401
     rmsnorm_forward,
     softmax_rows,
 )
+from . import solo_oracle_general  # noqa: F401,E402
+from .solo_oracle_general import exit_eval, general_bruteforce, general_fwd_bwd  # noqa: F401,E402
