@@ -19,6 +19,23 @@
  * gradients of its own trained readout W and gain (the FLOP table of the
  * paper's systems appendix: 2r per auxiliary readout, 3r for the terminal).
  *
+ * solo_readout_general extends this to everything Algorithm 1 and Eq. 2 put
+ * into a head's loss, and to the readout sources of the paper's variant
+ * tables (Section 3.3, table of readout sources; Appendix D, table of readout
+ * content and basis):
+ *
+ *     z_tv = tau_k <R_kv, g_k * n_t> + b_kv
+ *
+ * with a temperature tau_k and bias b_k per module (Alg. 1: the heads train
+ * (phi_k, tau_k, b_k), the terminal trains (W, b)), a gain g_k per module or
+ * one shared gain, and the heads' readout R_k (k < K-1) taken from W itself
+ * (SOLO), one other matrix shared by the heads (SOLO's copy from an earlier
+ * step when it is refreshed every S > 1 steps; RSHARE), or one matrix per
+ * head (RAND frozen, PRIV trained, ROT the caller's W R_k).  The terminal
+ * always reads W.  solo_readout_exit_eval is the forward pass alone: every
+ * exit's loss and top-1 prediction through its readout (early exit through
+ * the shared readout, Section 4).
+ *
  * All compute runs in hand-written HIP kernels on the caller's stream; the
  * T x V logit or probability matrix is never written to memory.
  */
@@ -32,9 +49,9 @@
 extern "C" {
 #endif
 
-#define SOLO_READOUT_ABI_VERSION 1
+#define SOLO_READOUT_ABI_VERSION 2
 
-/* Element type of h, gain, W and dh.  Statistics, exponentials and
+/* Element type of h, gain, W, Wbar and dh.  Statistics, exponentials and
  * accumulation are fp32 in both cases; the bf16 path multiplies bf16
  * operands (rounded to nearest even) on the matrix cores. */
 typedef enum {
@@ -48,8 +65,9 @@ typedef enum {
     SOLO_ERR_SHAPE = 2,     /* K, T or V < 1; d < 8, d % 8 != 0 or d > 4096; size overflow */
     SOLO_ERR_DTYPE = 3,     /* dtype is not a solo_dtype                                   */
     SOLO_ERR_ALIGN = 4,     /* a pointer violates the alignment stated below               */
-    SOLO_ERR_WORKSPACE = 5, /* workspace_bytes < solo_readout_workspace_size(...)           */
-    SOLO_ERR_ARG = 6,       /* eps < 0 or not finite; final_module_dW not 0 or 1           */
+    SOLO_ERR_WORKSPACE = 5, /* workspace_bytes below the size the workspace query returns  */
+    SOLO_ERR_ARG = 6,       /* eps < 0 or not finite; a flag not 0 or 1; flags that do not
+                               go together (see solo_readout_args)                       */
     SOLO_ERR_HIP = 7        /* a HIP runtime call or kernel launch failed                  */
 } solo_status;
 
@@ -60,9 +78,11 @@ int solo_readout_abi_version(void);
 const char* solo_status_string(int status);
 
 /*
- * Bytes of device workspace one call needs.  A function of (K, T, d, V,
- * dtype, final_module_dW) with no T*V term: the largest piece is a V x d
- * copy of the readout with the gain folded in.  Returns 0 for arguments that
+ * Bytes of device workspace one solo_readout_fwd_bwd call needs.  A function
+ * of (K, T, d, V, dtype, final_module_dW) with no T*V and no V*d term: per-token
+ * statistics, per-tile partial sums of the gain gradient and, on the
+ * matrix-core family, a bf16 copy of gain * h of the modules whose readout or
+ * bias gradient is computed (T*d*2 bytes each).  Returns 0 for arguments that
  * solo_readout_fwd_bwd would reject.
  */
 size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int final_module_dW);
@@ -70,8 +90,9 @@ size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int fi
 /*
  * Name of the kernel family one call with these sizes runs on:
  * "mfma" (bf16 matrix-core kernels) or "valu" (fp32 vector-ALU kernels,
- * used for SOLO_F32 and for bf16 widths the matrix-core kernels do not tile).
- * Returns "invalid" for arguments solo_readout_fwd_bwd would reject.
+ * used for SOLO_F32 and for bf16 widths the matrix-core kernels do not tile:
+ * d not a multiple of 256, or d > 2048).  Returns "invalid" for arguments
+ * solo_readout_fwd_bwd would reject.
  */
 const char* solo_readout_kernel_family(int K, int T, int d, int V, int dtype);
 
@@ -127,22 +148,25 @@ int solo_readout_fwd_bwd(int K, int T, int d, int V, int dtype, float eps,
                          void* hip_stream);
 
 /*
- * Stages of one call, in launch order (all on hip_stream).
+ * Stages of one call, in launch order (all on hip_stream).  Every stage
+ * event is recorded: right after its stage's work, or right after the
+ * previous event when the stage has no work in this call.
  */
 #define SOLO_NUM_STAGES 6
-/*   0  fold the gain into the readout copy (workspace)          */
-/*   1  per-token inverse RMS of h                                */
-/*   2  local-loss pass: logits, online log-sum-exp, dh (all K)   */
-/*   3  module losses (fixed-order mean of the per-token losses)  */
-/*   4  readout-gradient pass of module K-1 (dW, dgain partials)  */
-/*   5  dgain (fixed-order sum of the partials)                   */
+/*   0  per-token inverse RMS of h                                           */
+/*   1  local-loss pass (logits, online log-sum-exp, dh; all K), or the     */
+/*      forward-only exit evaluation                                         */
+/*   2  per-module sums in fixed order: losses, temperature gradients        */
+/*   3  readout-gradient pass (modules whose readout is trained), after the */
+/*      gain-scaled copy of h the matrix-core gradient passes stream         */
+/*   4  bias-gradient pass (modules whose bias but not readout is trained)   */
+/*   5  gain gradients (fixed-order sum of per-tile partials)                */
 
 /*
  * solo_readout_fwd_bwd, and for profiling: stage_events[i], if not NULL, is a
- * hipEvent_t that is recorded on hip_stream right after stage i has been
- * enqueued (stages 4 and 5 only run when final_module_dW = 1; their events
- * are then not recorded).  stage_events itself may be NULL.  Same arguments,
- * semantics and errors otherwise; a failed event record returns SOLO_ERR_HIP.
+ * hipEvent_t recorded on hip_stream as stated above.  stage_events itself
+ * may be NULL.  Same arguments, semantics and errors otherwise; a failed
+ * event record returns SOLO_ERR_HIP.
  */
 int solo_readout_fwd_bwd_profiled(int K, int T, int d, int V, int dtype, float eps,
                                   const void* h, const void* gain, const void* W,
@@ -151,6 +175,101 @@ int solo_readout_fwd_bwd_profiled(int K, int T, int d, int V, int dtype, float e
                                   float* dW, float* dgain,
                                   void* workspace, size_t workspace_bytes,
                                   void* hip_stream, void* const* stage_events);
+
+/*
+ * Arguments of solo_readout_general and solo_readout_exit_eval.  Zero-fill
+ * the struct, then set what the call uses; NULL pointers and 0 flags mean
+ * "absent".  Sizes, dtype, eps, h, targets, losses, row_loss, workspace and
+ * the stream are as in solo_readout_fwd_bwd.
+ *
+ * Inputs:
+ *   gain            [d] dtype (gain_per_module = 0: one gain, trained by the
+ *                   terminal only, read-only for the heads) or [K][d]
+ *                   (gain_per_module = 1: g_k owned by module k, every module
+ *                   gets its gradient); 16-byte aligned.
+ *   W               [V][d] dtype: the terminal readout (module K-1), 16-byte aligned.
+ *   Wbar            the heads' readout (modules 0..K-2), 16-byte aligned:
+ *                   NULL -> W itself (SOLO with the copy refreshed every step);
+ *                   [V][d] dtype with readout_per_head = 0 -> one matrix shared
+ *                   by the heads; [K-1][V][d] dtype with readout_per_head = 1
+ *                   -> one matrix per head.
+ *   tau             [K] float or NULL (every tau_k = 1; the paper's terminal
+ *                   has none, so pass tau[K-1] = 1 for that).  Not checked for
+ *                   finiteness.  4-byte aligned.
+ *   bias            [K][V] float or NULL (no bias).  4-byte aligned.
+ *
+ * Which gradients (fwd_bwd only; exit evaluation computes none):
+ *   final_module_dW      dW of the terminal, and with a shared gain its dgain.
+ *   heads_train_readout  PRIV: dWbar of every head; needs readout_per_head.
+ *   dtau != NULL         d losses[k] / d tau_k for every k (at tau = 1 if tau is NULL).
+ *   dbias != NULL        d losses[k] / d b_k for every k (at b = 0 if bias is NULL).
+ *                        The heads whose readout is not trained then run an
+ *                        extra logits-only pass (the bias-gradient pass): the
+ *                        column sums of the softmax need the final log-sum-exp.
+ *
+ * Outputs (fwd_bwd):
+ *   dh              [K][T][d] dtype, 16-byte aligned, required.
+ *   dW              [V][d] float, 16-byte aligned, required iff final_module_dW.
+ *   dWbar           [K-1][V][d] float, 16-byte aligned, required iff
+ *                   heads_train_readout and K > 1.
+ *   dgain           float, 4-byte aligned: [K][d] iff gain_per_module
+ *                   (required); else [d], required iff final_module_dW.
+ *   dtau            [K] float or NULL, 4-byte aligned.
+ *   dbias           [K][V] float or NULL, 4-byte aligned.
+ * Outputs (exit evaluation):
+ *   losses, row_loss as above; top1 [K][T] int32 or NULL, 4-byte aligned:
+ *   argmax_v z_tv in fp32 arithmetic, the lowest v on ties.
+ *
+ *   stage_events    NULL or SOLO_NUM_STAGES hipEvent_t, as for
+ *                   solo_readout_fwd_bwd_profiled.
+ *
+ * Semantics and errors as for solo_readout_fwd_bwd.  SOLO_ERR_ARG also for:
+ * a flag not 0 or 1, readout_per_head without Wbar, heads_train_readout
+ * without readout_per_head.
+ */
+typedef struct solo_readout_args {
+    int K, T, d, V;
+    int dtype;
+    float eps;
+    const void* h;
+    const void* gain;
+    const void* W;
+    const void* Wbar;
+    const float* tau;
+    const float* bias;
+    const int32_t* targets;
+    int gain_per_module;
+    int readout_per_head;
+    int final_module_dW;
+    int heads_train_readout;
+    float* losses;
+    float* row_loss;
+    void* dh;
+    float* dW;
+    float* dWbar;
+    float* dgain;
+    float* dtau;
+    float* dbias;
+    int32_t* top1;
+    void* workspace;
+    size_t workspace_bytes;
+    void* hip_stream;
+    void* const* stage_events;
+} solo_readout_args;
+
+/* Workspace bytes of solo_readout_general with these arguments (only the
+ * sizes, dtype, flags and which optional pointers are NULL matter); 0 if the
+ * call would be rejected for its sizes, dtype or flags. */
+size_t solo_readout_general_workspace_size(const solo_readout_args* args);
+
+/* Forward and local backward with every option above. */
+int solo_readout_general(const solo_readout_args* args);
+
+/* Workspace bytes of solo_readout_exit_eval (a function of K and T). */
+size_t solo_readout_exit_eval_workspace_size(const solo_readout_args* args);
+
+/* Forward-only exit evaluation: losses, row_loss and top1 of every module. */
+int solo_readout_exit_eval(const solo_readout_args* args);
 
 #ifdef __cplusplus
 }

@@ -23,6 +23,15 @@ __all__ = [
     "kernel_family",
     "readout_fwd_bwd",
     "readout_fwd_bwd_raw",
+    "SoloReadoutArgs",
+    "GeneralResult",
+    "EvalResult",
+    "general_workspace_size",
+    "exit_eval_workspace_size",
+    "readout_general",
+    "readout_general_raw",
+    "exit_eval",
+    "exit_eval_raw",
     "SOLO_BF16",
     "SOLO_F32",
     "STATUS",
@@ -45,6 +54,27 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
 
 ReadoutResult = collections.namedtuple("ReadoutResult", ["losses", "dh", "dW", "dgain", "row_loss"])
+GeneralResult = collections.namedtuple(
+    "GeneralResult", ["losses", "dh", "dW", "dWbar", "dgain", "dtau", "dbias", "row_loss"])
+EvalResult = collections.namedtuple("EvalResult", ["losses", "row_loss", "top1"])
+
+
+class SoloReadoutArgs(ctypes.Structure):
+    """Mirror of ``solo_readout_args`` (same field order and C alignment)."""
+
+    _fields_ = [
+        ("K", ctypes.c_int), ("T", ctypes.c_int), ("d", ctypes.c_int), ("V", ctypes.c_int),
+        ("dtype", ctypes.c_int), ("eps", ctypes.c_float),
+        ("h", ctypes.c_void_p), ("gain", ctypes.c_void_p), ("W", ctypes.c_void_p), ("Wbar", ctypes.c_void_p),
+        ("tau", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("targets", ctypes.c_void_p),
+        ("gain_per_module", ctypes.c_int), ("readout_per_head", ctypes.c_int),
+        ("final_module_dW", ctypes.c_int), ("heads_train_readout", ctypes.c_int),
+        ("losses", ctypes.c_void_p), ("row_loss", ctypes.c_void_p), ("dh", ctypes.c_void_p),
+        ("dW", ctypes.c_void_p), ("dWbar", ctypes.c_void_p), ("dgain", ctypes.c_void_p),
+        ("dtau", ctypes.c_void_p), ("dbias", ctypes.c_void_p), ("top1", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("hip_stream", ctypes.c_void_p), ("stage_events", ctypes.c_void_p),
+    ]
 
 
 class SoloError(RuntimeError):
@@ -90,6 +120,13 @@ def load_library():
     lib.solo_readout_fwd_bwd.argtypes = common
     lib.solo_readout_fwd_bwd_profiled.restype = c_int
     lib.solo_readout_fwd_bwd_profiled.argtypes = common + [ctypes.POINTER(vp)]
+    pargs = [ctypes.POINTER(SoloReadoutArgs)]
+    for name in ("solo_readout_general_workspace_size", "solo_readout_exit_eval_workspace_size"):
+        getattr(lib, name).restype = c_size
+        getattr(lib, name).argtypes = pargs
+    for name in ("solo_readout_general", "solo_readout_exit_eval"):
+        getattr(lib, name).restype = c_int
+        getattr(lib, name).argtypes = pargs
     _LIB = lib
     return lib
 
@@ -119,7 +156,7 @@ def kernel_family(K: int, T: int, d: int, V: int, dtype: int) -> str:
 
 
 NUM_STAGES = 6
-STAGE_NAMES = ["prep_readout", "row_rstd", "local_loss", "module_loss", "readout_grad", "dgain_reduce"]
+STAGE_NAMES = ["row_rstd", "local_loss", "module_sums", "readout_grad", "bias_grad", "dgain_reduce"]
 
 
 def readout_fwd_bwd_raw(K, T, d, V, dtype, eps, h, gain, W, targets, final_module_dW, losses, row_loss, dh, dW,
@@ -203,6 +240,153 @@ def readout_fwd_bwd(h, gain, W, targets, final_module_dW: bool = True, eps: floa
         out.losses.data_ptr(), out.row_loss.data_ptr() if out.row_loss is not None else 0, out.dh.data_ptr(),
         out.dW.data_ptr() if fdw else 0, out.dgain.data_ptr() if fdw else 0,
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), stream.cuda_stream, stage_events)
+    if st != 0:
+        raise SoloError(st, status_string(st))
+    return out
+
+
+def general_workspace_size(args: SoloReadoutArgs) -> int:
+    return int(load_library().solo_readout_general_workspace_size(ctypes.byref(args)))
+
+
+def exit_eval_workspace_size(args: SoloReadoutArgs) -> int:
+    return int(load_library().solo_readout_exit_eval_workspace_size(ctypes.byref(args)))
+
+
+def readout_general_raw(args: SoloReadoutArgs) -> int:
+    """Direct call with a filled SoloReadoutArgs; returns the status code."""
+    return int(load_library().solo_readout_general(ctypes.byref(args)))
+
+
+def exit_eval_raw(args: SoloReadoutArgs) -> int:
+    return int(load_library().solo_readout_exit_eval(ctypes.byref(args)))
+
+
+def _ptr(t):
+    return t.data_ptr() if t is not None else None
+
+
+def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps):
+    """Validate shapes and build the input part of SoloReadoutArgs (tensors kept alive by the caller)."""
+    import torch
+
+    if h.dim() != 3 or W.dim() != 2 or gain.dim() not in (1, 2) or targets.dim() != 2:
+        raise ValueError("expected h [K,T,d], gain [d] or [K,d], W [V,d], targets [K,T]")
+    K, T, d = h.shape
+    V = W.shape[0]
+    if W.shape[1] != d or gain.shape[-1] != d or (gain.dim() == 2 and gain.shape[0] != K) \
+            or tuple(targets.shape) != (K, T):
+        raise ValueError(f"shape mismatch: h {tuple(h.shape)}, gain {tuple(gain.shape)}, W {tuple(W.shape)}, "
+                         f"targets {tuple(targets.shape)}")
+    if Wbar is not None and tuple(Wbar.shape) not in ((V, d), (K - 1, V, d)):
+        raise ValueError(f"Wbar must be [V,d] or [K-1,V,d], got {tuple(Wbar.shape)}")
+    if tau is not None and tuple(tau.shape) != (K,):
+        raise ValueError("tau must be [K]")
+    if bias is not None and tuple(bias.shape) != (K, V):
+        raise ValueError("bias must be [K,V]")
+    dts = {h.dtype, gain.dtype, W.dtype} | ({Wbar.dtype} if Wbar is not None else set())
+    if len(dts) != 1:
+        raise TypeError("h, gain, W and Wbar must share one dtype")
+    for t in (h, gain, W, targets, Wbar, tau, bias):
+        if t is not None and not t.is_cuda:
+            raise ValueError("all inputs must be GPU tensors")
+    keep = {
+        "h": h.contiguous(), "gain": gain.contiguous(), "W": W.contiguous(),
+        "Wbar": Wbar.contiguous() if Wbar is not None else None,
+        "tau": tau.to(torch.float32).contiguous() if tau is not None else None,
+        "bias": bias.to(torch.float32).contiguous() if bias is not None else None,
+        "targets": targets.to(torch.int32).contiguous(),
+    }
+    a = SoloReadoutArgs()
+    a.K, a.T, a.d, a.V = K, T, d, V
+    a.dtype = _dtype_code(h.dtype)
+    a.eps = float(eps)
+    for name in ("h", "gain", "W", "Wbar", "tau", "bias", "targets"):
+        setattr(a, name, _ptr(keep[name]))
+    a.gain_per_module = int(gain.dim() == 2)
+    a.readout_per_head = int(Wbar is not None and Wbar.dim() == 3)
+    return a, keep
+
+
+def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, final_module_dW: bool = True,
+                    heads_train_readout: bool = False, want_dtau: bool = False, want_dbias: bool = False,
+                    eps: float = 1e-6, row_loss: bool = False, workspace=None, stream=None,
+                    stage_events=None) -> GeneralResult:
+    """The loss with temperatures, biases, per-module gains and readout sources
+    (``solo_readout_general``).  ``gain`` [d] or [K, d]; ``Wbar`` None, [V, d] or
+    [K-1, V, d] (same dtype as h); ``tau`` [K] and ``bias`` [K, V] float32 or None.
+    Returns GeneralResult; gradients that were not requested are None.
+    """
+    import torch
+
+    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
+    K, T, d, V = a.K, a.T, a.d, a.V
+    dev = h.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    fdw = bool(final_module_dW)
+    priv = bool(heads_train_readout)
+    out = GeneralResult(
+        losses=torch.empty(K, **f32),
+        dh=torch.empty_like(keep["h"]),
+        dW=torch.empty((V, d), **f32) if fdw else None,
+        dWbar=torch.empty((K - 1, V, d), **f32) if (priv and K > 1) else None,
+        dgain=(torch.empty((K, d), **f32) if a.gain_per_module else (torch.empty(d, **f32) if fdw else None)),
+        dtau=torch.empty(K, **f32) if want_dtau else None,
+        dbias=torch.empty((K, V), **f32) if want_dbias else None,
+        row_loss=torch.empty((K, T), **f32) if row_loss else None,
+    )
+    a.final_module_dW = int(fdw)
+    a.heads_train_readout = int(priv)
+    for name in ("losses", "dh", "dW", "dWbar", "dgain", "dtau", "dbias", "row_loss"):
+        setattr(a, name, _ptr(getattr(out, name)))
+    ws_bytes = general_workspace_size(a)
+    if ws_bytes == 0:
+        raise SoloError(STATUS["SOLO_ERR_SHAPE"], status_string(STATUS["SOLO_ERR_SHAPE"]))
+    if workspace is None or workspace.numel() * workspace.element_size() < ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    a.workspace = workspace.data_ptr()
+    a.workspace_bytes = workspace.numel() * workspace.element_size()
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    a.hip_stream = stream.cuda_stream or None
+    evs = None
+    if stage_events is not None:
+        evs = (ctypes.c_void_p * NUM_STAGES)(*[(e or None) for e in stage_events])
+        a.stage_events = ctypes.cast(evs, ctypes.c_void_p)
+    st = readout_general_raw(a)
+    if st != 0:
+        raise SoloError(st, status_string(st))
+    return out
+
+
+def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float = 1e-6, row_loss: bool = True,
+              top1: bool = True, workspace=None, stream=None) -> EvalResult:
+    """Forward-only exit evaluation (``solo_readout_exit_eval``): losses [K],
+    row_loss [K, T] and top1 [K, T] int32 (argmax of the logits, lowest index on ties)."""
+    import torch
+
+    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
+    K, T = a.K, a.T
+    dev = h.device
+    out = EvalResult(
+        losses=torch.empty(K, dtype=torch.float32, device=dev),
+        row_loss=torch.empty((K, T), dtype=torch.float32, device=dev) if row_loss else None,
+        top1=torch.empty((K, T), dtype=torch.int32, device=dev) if top1 else None,
+    )
+    a.losses = _ptr(out.losses)
+    a.row_loss = _ptr(out.row_loss)
+    a.top1 = _ptr(out.top1)
+    ws_bytes = exit_eval_workspace_size(a)
+    if ws_bytes == 0:
+        raise SoloError(STATUS["SOLO_ERR_SHAPE"], status_string(STATUS["SOLO_ERR_SHAPE"]))
+    if workspace is None or workspace.numel() * workspace.element_size() < ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    a.workspace = workspace.data_ptr()
+    a.workspace_bytes = workspace.numel() * workspace.element_size()
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    a.hip_stream = stream.cuda_stream or None
+    st = exit_eval_raw(a)
     if st != 0:
         raise SoloError(st, status_string(st))
     return out

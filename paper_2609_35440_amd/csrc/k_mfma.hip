@@ -1,19 +1,33 @@
 // Fused matrix-core passes of the SOLO shared-readout loss (bf16 operands, fp32
 // accumulate) for gfx950.
 //
-// Both passes have the shape "logit tile -> elementwise -> second product":
+// Every pass has the shape "logit tile -> elementwise -> (second product)".
+// Module k predicts through its readout R_k (the terminal's W for k = K-1,
+// the heads' read-only copy otherwise), its gain g_k, temperature tau_k and
+// bias b_k (Eq. 2 of the paper, with the bias of Algorithm 1):
 //
-//   local-loss pass (every module, Eq. 2 and Eq. 3 of the paper):
-//     stationary X = 32 rows t of h_k, streamed Y = the readout rows v,
-//     z_tv = r_t <Wg_v, h_t>, online (max, sum-exp) per row, and
-//     acc_t += sum_v exp(z_tv - m_t) Wg_v        (Wg = W diag(gain))
-//     so that dn_t = (acc_t / s_t - Wg_{y_t}) / T at the end, followed by the
-//     RMSNorm backward.  The T x V logits and probabilities stay on chip.
+//   z_tv = tau_k r_t <R_kv, g_k * h_t> + b_kv
 //
-//   readout-gradient pass (final module only; the copies get no gradient):
-//     stationary X = 32 readout rows v, streamed Y = the rows t of h_{K-1},
-//     delta_tv = (exp(z_tv - lse_t) - [v = y_t]) / T and
-//     D_v += sum_t delta_tv r_t h_t,  dW_v = gain * D_v,  dgain += W_v * D_v.
+//   local-loss pass (every module; Eq. 2 and Eq. 3):
+//     stationary X = 32 rows t of g_k * h_k, streamed Y = the readout rows v,
+//     online (max, sum-exp) per row, and acc_t += sum_v exp(z_tv - m_t) R_kv,
+//     so that dhhat_t = tau_k (acc_t / s_t - R_{k,y_t}) / T at the end, followed
+//     by the RMSNorm backward and, for a module that trains its gain, the
+//     tile's partial of dgain = sum_t dhhat_t * n_t.  The T x V logits and
+//     probabilities stay on chip.
+//
+//   exit evaluation: the same without the second product; the top-1 of each
+//     row (lowest index on ties) next to its loss.
+//
+//   readout-gradient pass (modules whose readout is trained):
+//     stationary X = 32 readout rows v, streamed Y = the rows t of g_k * h_k
+//     (a copy rounded like the local-loss pass's stationary tile, so both
+//     passes multiply the same operands), delta_tv = (exp(z_tv - lse_t) -
+//     [v = y_t]) / T and dR_v = sum_t delta_tv tau_k r_t (g_k * h_t),
+//     db_v = sum_t delta_tv.
+//
+//   bias-gradient pass: the readout-gradient pass without the second product,
+//     for modules whose bias is trained but whose readout is not.
 //
 // Work split: a workgroup of 8 waves owns the 32 stationary rows; wave w owns
 // the d/8 columns [w d/8, (w+1) d/8).  Per chunk of 16 streamed rows, every
@@ -38,20 +52,32 @@ constexpr int XR = kMfmaRows;  // stationary rows per workgroup (32)
 constexpr int YC = layout::YC;  // streamed rows per chunk
 constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: conflict-free 16 B writes
 
+enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
+
 template <int DS>
 struct Geo : layout::Geo<DS> {
     static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
     static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
     static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
-    static constexpr int TOTAL = 2 * YBUF + NW * XR * PP * 4 + XR * YC * 2 + 2 * XR * 4 + NW * XR * 4;
+    static constexpr int TOTAL = 2 * YBUF + NW * XR * PP * 4 + XR * YC * 2 + 2 * XR * 4 + NW * XR * 4 + 4 * YC * 4;
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
-// MODE 0: local-loss pass, grid (ceil(T/32), K).
-// MODE 1: readout-gradient pass of module K-1, grid (ceil(V/32)).
-template <int MODE, int DS>
+__device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
+    return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
+}
+
+// MODE LOCAL / EVAL: grid (ceil(T/32), K); module k = blockIdx.y.
+// MODE RGRAD / BGRAD: grid (ceil(V/32), nmod); module k = m0 + blockIdx.y.
+// EXT (LOCAL only): the variant with per-chunk biases and the running sums
+// of the temperature gradient; EVAL always handles biases.
+template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     using G = Geo<DS>;
+    constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
+    constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
+    constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
+    constexpr bool DT = MODE == LOCAL && EXT;               // temperature-gradient sums
     // the stream of a chunk is issued in batches [0, kDma1), [kDma1, kDma2), [kDma2, NI)
     constexpr int kDma1 = (3 * G::NI + 7) / 8, kDma2 = (6 * G::NI + 7) / 8;
     // Separate LDS objects, so that the compiler can tell the chunk being read
@@ -63,7 +89,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     __shared__ float abuf[XR];
     __shared__ float sbuf[XR];
     __shared__ float cbuf[NW * XR];
-    __shared__ __attribute__((aligned(16))) float recA[YC * 4];  // readout-gradient pass: per-token records
+    // per-chunk side data streamed next to the chunk: the per-token records
+    // (readout-/bias-gradient passes) or the chunk's 16 biases (local loss)
+    __shared__ __attribute__((aligned(16))) float recA[YC * 4];
     __shared__ __attribute__((aligned(16))) float recB[YC * 4];
 
     const int lane = threadIdx.x & 63;
@@ -71,15 +99,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int d = a.d;
     const int js = w * DS;
     const int x0 = blockIdx.x * XR;
-    const int k = (MODE == 0) ? (int)blockIdx.y : a.K - 1;
+    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
     const long long modoff = (long long)k * a.T;
+    const float tau_k = a.tau ? a.tau[k] : 1.f;
 
     const bf16* __restrict__ hk = (const bf16*)a.h + modoff * d;
-    const bf16* __restrict__ Wg = (const bf16*)a.Wg;
-    const bf16* __restrict__ X = (MODE == 0) ? hk : Wg;
-    const bf16* __restrict__ Y = (MODE == 0) ? Wg : hk;
-    const int nX = (MODE == 0) ? a.T : a.V;
-    const int nY = (MODE == 0) ? a.V : a.T;
+    const bf16* __restrict__ Rk = readout_of(a, k);
+    const bf16* __restrict__ gk = (const bf16*)a.gain + (long long)k * a.g_stride;
+    const bf16* __restrict__ X = LL ? hk : Rk;
+    const bf16* __restrict__ Y = LL ? Rk : (const bf16*)a.hg + (long long)(k - a.hg_m0) * a.T * d;
+    const int nX = LL ? a.T : a.V;
+    const int nY = LL ? a.V : a.T;
     const int nchunks = (nY + YC - 1) / YC;
 
     LDS_AS char* sliceA = (LDS_AS char*)(LDS_AS void*)ybufA + w * G::SLICE;
@@ -88,64 +118,85 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     // per-lane scalars of the rows this wave finishes in the elementwise step
     const int xo = 4 * w + (lane >> 4);   // stationary row (0..31) owned in the elementwise step
     const int yy = lane & 15;             // streamed row within the chunk
-    float own_r = 0.f;                    // MODE 0: r_t of row xo
-    int own_tgt = -1;                     // MODE 0: target of row xo
-    if (MODE == 0 && x0 + xo < nX) {
-        own_r = a.rstd[modoff + x0 + xo];
+    float own_r2 = 0.f;                   // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
+    int own_tgt = -1;                     // LL: target of row xo
+    if (LL && x0 + xo < nX) {
+        own_r2 = a.rstd[modoff + x0 + xo] * tau_k * kLog2e;
         own_tgt = a.targets[modoff + x0 + xo];
     }
-    const float own_r2 = own_r * kLog2e;
+    // readout-/bias-gradient passes: bias of the stationary readout row, base 2
+    float bx2 = 0.f;
+    if (!LL && a.bias && x0 + xo < nX) bx2 = a.bias[(long long)k * a.V + x0 + xo] * kLog2e;
+    const bool has_bias = a.bias != nullptr;
 
     ChunkStream<DS> stream;
     stream.init(d, js, lane);
     // first chunk in flight before the stationary operand is read
     const unsigned sliceA_u = lds_addr(sliceA), sliceB_u = lds_addr(sliceB);
     stream.issue(Y, nY, d, 0, sliceA_u);
-    // readout-gradient pass: the 16 per-token records {lse, rstd, target, 0}
-    // of a chunk stream into recA / recB next to the chunk itself
     const unsigned recA_u = lds_addr((LDS_AS char*)(LDS_AS void*)recA);
     const unsigned recB_u = lds_addr((LDS_AS char*)(LDS_AS void*)recB);
-    auto issue_rec = [&](int y0, unsigned dst) __attribute__((always_inline)) {
-        if (MODE == 1 && w == 0 && lane < YC) {
-            const int rows = nY - y0;
+    auto issue_side = [&](int y0, unsigned dst) __attribute__((always_inline)) {
+        const int rows = nY - y0;
+        if (!LL && w == 0 && lane < YC) {
+            // the 16 per-token records of the chunk
             const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
-            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (long long)y0, rem), dst, lane * 16);
+            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, lane * 16);
+        }
+        if (BZ && has_bias && w == 0 && lane < YC) {
+            // the 16 biases of the chunk (zeros past the vocabulary)
+            const unsigned rem = rows > 0 ? (unsigned)rows * 4u : 0u;
+            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, lane * 4);
         }
     };
-    issue_rec(0, recA_u);
+    issue_side(0, recA_u);
 
-    // stationary operand: B of the 16x16x32 logit product, lane holds
+    // stationary operand (local loss and exit evaluation: times the gain,
+    // rounded once): B of the 16x16x32 logit product, lane holds
     // X[x0 + 16 xb + lane%16][js + 32 kk + 8 (lane/16) .. +7]
     bf16x8 xr[2][G::NK];
 #pragma unroll
-    for (int xb = 0; xb < 2; ++xb) {
-        const int xrow = x0 + 16 * xb + (lane & 15);
+    for (int kk = 0; kk < G::NK; ++kk) {
+        const int j0 = js + 32 * kk + 8 * (lane >> 4);
+        const bf16x8 gv = *(const bf16x8*)(gk + j0);
 #pragma unroll
-        for (int kk = 0; kk < G::NK; ++kk) {
+        for (int xb = 0; xb < 2; ++xb) {
+            const int xrow = x0 + 16 * xb + (lane & 15);
+            bf16x8 xv;
             if (xrow < nX) {
-                xr[xb][kk] = *(const bf16x8*)(X + (long long)xrow * d + js + 32 * kk + 8 * (lane >> 4));
+                xv = *(const bf16x8*)(X + (long long)xrow * d + j0);
             } else {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) xr[xb][kk][e] = (bf16)0.f;
+                for (int e = 0; e < 8; ++e) xv[e] = (bf16)0.f;
+            }
+            if (LL) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xr[xb][kk][e] = (bf16)((float)xv[e] * (float)gv[e]);
+            } else {
+                xr[xb][kk] = xv;
             }
         }
     }
 
-    f32x16 acc[G::NB];
+    f32x16 acc[PC ? G::NB : 1];
 #pragma unroll
-    for (int b = 0; b < G::NB; ++b)
+    for (int b = 0; b < (PC ? G::NB : 1); ++b)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[b][i] = 0.f;
 
-    // online softmax state (MODE 0, base 2), per lane: row xo, streamed column yy
+    // online softmax state (LL, base 2), per lane: row xo, streamed column yy
     float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
+    float su_part = 0.f, sy_part = 0.f;   // DT: sum_v e^(z - m) sxy_v, and sxy of the target (u = r sxy)
+    float best = -INFINITY;               // EVAL: largest logit seen by this lane, and its column
+    int best_v = -1;
+    float db_part = 0.f;                  // RGRAD / BGRAD: sum_t (p - onehot) for row xo
 
     // per-lane parts of the LDS addresses; the unrolled loops add 64 * kk or 64 * b
     const int a_off = layout::rowread_off<DS>(lane);
     const int c_lo = layout::trread_off<DS>(lane, 0);
     const int c_hi = layout::trread_off<DS>(lane, 1);
 
-    auto step = [&](LDS_AS char* cur, unsigned nxt, LDS_AS float* rec, unsigned rec_nxt, int c)
+    auto step = [&](LDS_AS char* cur, unsigned nxt, LDS_AS float* side, unsigned side_nxt, int c)
                     __attribute__((always_inline)) {
         const int y0 = c * YC;
         const bool more = c + 1 < nchunks;
@@ -156,18 +207,22 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // whose stream is issued in three batches (here, after these products
         // and after the elementwise step) so that neither the texture unit's
         // queue nor the LDS write port sees the whole chunk at once.
-        bf16x8 ay[G::NK];
+        // (the extended variant at the widest slices holds 6 of them at a time:
+        // each later read refills the registers of the products just issued)
+        constexpr int RA = (DT && G::NK > 6) ? 6 : G::NK;
+        bf16x8 ay[RA];
 #pragma unroll
-        for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
+        for (int kk = 0; kk < RA; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
         if (more) {
             stream.template issue_range<0, kDma1>(nrs, d, nxt);
-            issue_rec(y0 + YC, rec_nxt);
+            issue_side(y0 + YC, side_nxt);
         }
         f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
-            S0 = mfma16(ay[kk], xr[0][kk], S0);
-            S1 = mfma16(ay[kk], xr[1][kk], S1);
+            S0 = mfma16(ay[kk % RA], xr[0][kk], S0);
+            S1 = mfma16(ay[kk % RA], xr[1][kk], S1);
+            if (kk + RA < G::NK) ay[kk % RA] = *(LDS_AS bf16x8*)(cur + a_off + 64 * (kk + RA));
         }
         if (more) stream.template issue_range<kDma1, kDma2>(nrs, d, nxt);
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
@@ -182,11 +237,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         static_assert(NW == 8, "partial-sum tree");
         const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
         const int yg = y0 + yy;
-        float gval;
-        if (MODE == 0) {
+        float gval = 0.f;
+        if (LL) {
             // columns past the end of the vocabulary get z = -inf (an additive
             // mask rather than a branch, so the partial reads stay unconditional)
-            const float ymask = (yg < nY) ? 0.f : -INFINITY;
+            float ymask = (yg < nY) ? 0.f : -INFINITY;
+            if (BZ && has_bias) ymask += side[yy] * kLog2e;
             const float zc = __builtin_fmaf(sxy, own_r2, ymask);
             float alpha = 1.f;
             if (__builtin_expect(__any(zc > m_run + kLazyThresh2), 0)) {  // wave-uniform
@@ -194,48 +250,62 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (cmax > m_run + kLazyThresh2) {
                     alpha = __builtin_amdgcn_exp2f(m_run - cmax);
                     s_part *= alpha;
+                    if (DT) su_part *= alpha;
                     m_run = cmax;
                 }
             }
             const float p = __builtin_amdgcn_exp2f(zc - m_run);
             s_part += p;
-            if (yg == own_tgt) zy_part = zc;
+            if (DT) su_part = __builtin_fmaf(p, sxy, su_part);
+            if (yg == own_tgt) {
+                zy_part = zc;
+                if (DT) sy_part = sxy;
+            }
+            if (MODE == EVAL && zc > best) {  // strict: the first (lowest) column keeps a tie
+                best = zc;
+                best_v = yg;
+            }
             gval = p;
-            abuf[xo] = alpha;  // the 16 lanes of a row store the same value
+            if (MODE == LOCAL) abuf[xo] = alpha;  // the 16 lanes of a row store the same value
         } else {
-            // record {lse log2 e, r log2 e, target, r / T}; rows past the end
-            // read as zeros and give gval = 0
-            const f32x4 r4 = *(LDS_AS f32x4*)(rec + 4 * yy);
-            const float p = __builtin_amdgcn_exp2f(sxy * r4[1] - r4[0]);
-            gval = (p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f)) * r4[3];
+            // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
+            // the end of the module read as zeros and are masked
+            const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2 - r4[0]));
+            // (a padded token's zero record would match readout row 0 as its target)
+            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f) : 0.f;
+            gval = dlt * r4[3];
+            db_part += dlt;
         }
-        gbuf[xo * YC + yy] = (bf16)gval;
+        if (PC) gbuf[xo * YC + yy] = (bf16)gval;
         if (more) stream.template issue_range<kDma2, G::NI>(nrs, d, nxt);
         lds_barrier();
 
-        // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
-        const bf16x8 gfrag = *(bf16x8*)(gbuf + (lane & 31) * YC + 8 * (lane >> 5));
-        if (MODE == 0) {
-            const float al = abuf[lane & 31];
-            if (__any(al != 1.f)) {
+        if (PC) {
+            // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
+            const bf16x8 gfrag = *(bf16x8*)(gbuf + (lane & 31) * YC + 8 * (lane >> 5));
+            if (MODE == LOCAL) {
+                const float al = abuf[lane & 31];
+                if (__any(al != 1.f)) {
 #pragma unroll
-                for (int b = 0; b < G::NB; ++b)
+                    for (int b = 0; b < G::NB; ++b)
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) acc[b][i] *= al;
+                        for (int i = 0; i < 16; ++i) acc[b][i] *= al;
+                }
             }
-        }
-        bf16x4 tlo[G::NB], thi[G::NB];
+            bf16x4 tlo[G::NB], thi[G::NB];
 #pragma unroll
-        for (int b = 0; b < G::NB; ++b) {
-            tlo[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_lo + 64 * b));
-            thi[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_hi + 64 * b));
-        }
+            for (int b = 0; b < G::NB; ++b) {
+                tlo[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_lo + 64 * b));
+                thi[b] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS_AS bf16x4*)(cur + c_hi + 64 * b));
+            }
 #pragma unroll
-        for (int b = 0; b < G::NB; ++b) {
-            bf16x8 at;
-            at[0] = tlo[b][0]; at[1] = tlo[b][1]; at[2] = tlo[b][2]; at[3] = tlo[b][3];
-            at[4] = thi[b][0]; at[5] = thi[b][1]; at[6] = thi[b][2]; at[7] = thi[b][3];
-            acc[b] = mfma32(at, gfrag, acc[b]);
+            for (int b = 0; b < G::NB; ++b) {
+                bf16x8 at;
+                at[0] = tlo[b][0]; at[1] = tlo[b][1]; at[2] = tlo[b][2]; at[3] = tlo[b][3];
+                at[4] = thi[b][0]; at[5] = thi[b][1]; at[6] = thi[b][2]; at[7] = thi[b][3];
+                acc[PC ? b : 0] = mfma32(at, gfrag, acc[PC ? b : 0]);
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
         wait_vm();
@@ -251,51 +321,79 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     //      j = js + 32 b + 8 (i/4) + 4 (lane/32) + i%4 for i = 0..15
     const int ex = lane & 31;
     const int ehh = lane >> 5;
-    if (MODE == 0) {
+    if (LL) {
         // finish the online softmax of rows 4w..4w+3
-        float s = s_part, zy = zy_part;
-        s = row16_sum(s);
-        zy = row16_sum(zy);
+        const float s = row16_sum(s_part);
+        const float zy = row16_sum(zy_part);
+        const float su = DT ? row16_sum(su_part) : 0.f;
+        const float sy = DT ? row16_sum(sy_part) : 0.f;
+        if (MODE == EVAL) {
+            // argmax over the 16 lanes of the row: larger logit, then lower column
+#pragma unroll
+            for (int off = 1; off < 16; off <<= 1) {
+                const float ob = __shfl_xor(best, off, 64);
+                const int ov = __shfl_xor(best_v, off, 64);
+                if (ob > best || (ob == best && (unsigned)ov < (unsigned)best_v)) {
+                    best = ob;
+                    best_v = ov;
+                }
+            }
+        }
         if (yy == 0) {
+            const float r_row = (x0 + xo < nX) ? a.rstd[modoff + x0 + xo] : 0.f;
             const float lse2 = m_run + __log2f(s);
             const bool tok = own_tgt >= 0 && own_tgt < nY;
             const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
             if (x0 + xo < nX) {
-                a.lse[modoff + x0 + xo] = lse2 * kLn2;
-                a.rowloss[modoff + x0 + xo] = rl;
-                if (a.rowrec && k == a.K - 1) {
-                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), own_r * a.inv_T};
-                    *(f32x4*)(a.rowrec + 4 * (long long)(x0 + xo)) = rec4;
+                const long long t = modoff + x0 + xo;
+                a.lse[t] = lse2 * kLn2;
+                a.rowloss[t] = rl;
+                if (MODE == EVAL && a.top1) a.top1[t] = best_v;
+                if (MODE == LOCAL && a.rowrec) {
+                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), r_row * tau_k * a.inv_T};
+                    *(f32x4*)(a.rowrec + 4 * t) = rec4;
                 }
+                // d loss / d tau per token: (sum_v p_v u_v - u_y) / T with u = r sxy
+                if (DT && a.rowdtau) a.rowdtau[t] = tok ? r_row * (su / s - sy) * a.inv_T : 0.f;
             }
             sbuf[xo] = 1.f / s;
         }
+    }
+    if (MODE == LOCAL) {
         __syncthreads();
-
         const int xg = x0 + ex;
         const bool xok = xg < nX;
         const float rx = xok ? a.rstd[modoff + xg] : 0.f;
         const int tgt = xok ? a.targets[modoff + xg] : -1;
         const bool tok = tgt >= 0 && tgt < nY;
         const float inv_s = sbuf[ex];
+        const float scale = tau_k * a.inv_T;
         const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
-        const bf16* wrow = Wg + (long long)(tok ? tgt : 0) * d;
+        const bf16* wrow = Rk + (long long)(tok ? tgt : 0) * d;
+        const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
+        float* dgp = want_dg ? a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d
+                             : nullptr;
+        // sweep 1: acc <- dhhat = tau (acc / s - R_y) / T and the row sums of dn * n (dn = g dhhat, n = r h)
         float cp = 0.f;
 #pragma unroll
-        for (int b = 0; b < G::NB; ++b) {
+        for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
             for (int i4 = 0; i4 < 4; ++i4) {
                 const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                u16x4 hv = {0, 0, 0, 0}, wv = {0, 0, 0, 0};
-                if (xok) hv = *(const u16x4*)(hrow + j);
-                if (tok) wv = *(const u16x4*)(wrow + j);
+                // unconditional loads (the row pointers are clamped to row 0), masked
+                // afterwards: no control flow inside the sweep
+                const u16x4 hv = *(const u16x4*)(hrow + j);
+                const u16x4 wv = *(const u16x4*)(wrow + j);
+                const u16x4 gv = *(const u16x4*)(gk + j);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float dn = (acc[b][4 * i4 + e] * inv_s - bf16_bits_to_f32(wv[e])) * a.inv_T;
-                    cp += dn * (rx * bf16_bits_to_f32(hv[e]));
-                    acc[b][4 * i4 + e] = dn;
+                    const float wy = tok ? bf16_bits_to_f32(wv[e]) : 0.f;
+                    const float dhat = (acc[b][4 * i4 + e] * inv_s - wy) * scale;
+                    cp += bf16_bits_to_f32(gv[e]) * dhat * (rx * bf16_bits_to_f32(hv[e]));
+                    acc[b][4 * i4 + e] = dhat;
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);  // one block's loads at a time
         }
         cp += __shfl_xor(cp, 32, 64);
         if (ehh == 0) cbuf[w * XR + ex] = cp;
@@ -304,85 +402,94 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + ex];
         const float cmean = csum / (float)d;
+
+        // sweep 2: dh = r (dn - c n)
         if (xok) {
             bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
 #pragma unroll
-            for (int b = 0; b < G::NB; ++b) {
+            for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
                 for (int i4 = 0; i4 < 4; ++i4) {
                     const int j = js + 32 * b + 8 * i4 + 4 * ehh;
                     const u16x4 hv = *(const u16x4*)(hrow + j);
+                    const u16x4 gv = *(const u16x4*)(gk + j);
                     bf16x4 o;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float n = rx * bf16_bits_to_f32(hv[e]);
-                        o[e] = (bf16)(rx * (acc[b][4 * i4 + e] - cmean * n));
+                        o[e] = (bf16)(rx * (bf16_bits_to_f32(gv[e]) * acc[b][4 * i4 + e] - cmean * n));
                     }
                     *(bf16x4*)(dhrow + j) = o;
                 }
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
-    } else {
+        // sweep 3, for a module that trains its gain: the tile's partial sums
+        // of dhhat * n over its 32 rows (the 16-lane row, then the other row
+        // of the half-wave)
+        if (want_dg) {
+#pragma unroll
+            for (int b = 0; b < (PC ? G::NB : 1); ++b) {
+#pragma unroll
+                for (int i4 = 0; i4 < 4; ++i4) {
+                    const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                    const u16x4 hv = *(const u16x4*)(hrow + j);  // rx = 0 masks rows past the end
+                    f32x4 pv;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float t = row16_sum(acc[b][4 * i4 + e] * (rx * bf16_bits_to_f32(hv[e])));
+                        pv[e] = t + __shfl_xor(t, 16, 64);
+                    }
+                    if (ex == 0) *(f32x4*)(dgp + j) = pv;
+                }
+            }
+        }
+    }
+    if (!LL) {
+        // bias gradient of the stationary readout rows: sum over the 16 lanes of the row
+        const float db = row16_sum(db_part);
+        if (a.dbias && yy == 0 && x0 + xo < nX) a.dbias[(long long)k * a.V + x0 + xo] = db * a.inv_T;
+    }
+    if (MODE == RGRAD) {
+        // dR_v = D_v
         const int v = x0 + ex;
         const bool vok = v < nX;
-        const bf16* wrow = (const bf16*)a.W + (long long)(vok ? v : 0) * d;
-        const bf16* gain = (const bf16*)a.gain;
-        float* dwrow = a.dW + (long long)(vok ? v : 0) * d;
-        float* dgp = a.dgain_part + (long long)blockIdx.x * d;
+        float* dR = (k == a.K - 1) ? a.dWt : a.dWh + (long long)k * a.V * d;
+        float* dwrow = dR + (long long)(vok ? v : 0) * d;
 #pragma unroll
-        for (int b = 0; b < G::NB; ++b) {
+        for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
             for (int i4 = 0; i4 < 4; ++i4) {
                 const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                const u16x4 gv = *(const u16x4*)(gain + j);
-                u16x4 wv = {0, 0, 0, 0};
-                if (vok) wv = *(const u16x4*)(wrow + j);
                 f32x4 o;
-                float pr[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float D = acc[b][4 * i4 + e];
-                    o[e] = bf16_bits_to_f32(gv[e]) * D;
-                    pr[e] = bf16_bits_to_f32(wv[e]) * D;
-                }
+                for (int e = 0; e < 4; ++e) o[e] = acc[b][4 * i4 + e];
                 if (vok) *(f32x4*)(dwrow + j) = o;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float t = pr[e];
-                    t += __shfl_xor(t, 1, 64);
-                    t += __shfl_xor(t, 2, 64);
-                    t += __shfl_xor(t, 4, 64);
-                    t += __shfl_xor(t, 8, 64);
-                    t += __shfl_xor(t, 16, 64);
-                    pr[e] = t;
-                }
-                if (ex == 0) {
-                    f32x4 pv = {pr[0], pr[1], pr[2], pr[3]};
-                    *(f32x4*)(dgp + j) = pv;
-                }
             }
         }
     }
 }
 
-template <int MODE, int DS>
-hipError_t launch_ds(const FusedArgs& a, hipStream_t s) {
-    dim3 grid = (MODE == 0) ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K) : dim3((unsigned)((a.V + XR - 1) / XR));
-    hipLaunchKernelGGL((k_fused<MODE, DS>), grid, dim3(NTHR), 0, s, a);
+template <int MODE, int DS, bool EXT>
+hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
+    const bool ll = MODE == LOCAL || MODE == EVAL;
+    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
+                   : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
+    hipLaunchKernelGGL((k_fused<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
     return hipGetLastError();
 }
 
-template <int MODE>
-hipError_t launch_mode(const FusedArgs& a, hipStream_t s) {
+template <int MODE, bool EXT>
+hipError_t launch_mode(const FusedArgs& a, int nmod, hipStream_t s) {
     switch (a.d / NW) {
-        case 32: return launch_ds<MODE, 32>(a, s);
-        case 64: return launch_ds<MODE, 64>(a, s);
-        case 96: return launch_ds<MODE, 96>(a, s);
-        case 128: return launch_ds<MODE, 128>(a, s);
-        case 160: return launch_ds<MODE, 160>(a, s);
-        case 192: return launch_ds<MODE, 192>(a, s);
-        case 224: return launch_ds<MODE, 224>(a, s);
-        case 256: return launch_ds<MODE, 256>(a, s);
+        case 32: return launch_ds<MODE, 32, EXT>(a, nmod, s);
+        case 64: return launch_ds<MODE, 64, EXT>(a, nmod, s);
+        case 96: return launch_ds<MODE, 96, EXT>(a, nmod, s);
+        case 128: return launch_ds<MODE, 128, EXT>(a, nmod, s);
+        case 160: return launch_ds<MODE, 160, EXT>(a, nmod, s);
+        case 192: return launch_ds<MODE, 192, EXT>(a, nmod, s);
+        case 224: return launch_ds<MODE, 224, EXT>(a, nmod, s);
+        case 256: return launch_ds<MODE, 256, EXT>(a, nmod, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -391,7 +498,15 @@ hipError_t launch_mode(const FusedArgs& a, hipStream_t s) {
 
 bool mfma_supported(int dtype, int d) { return dtype == 0 && d % (NW * 32) == 0 && d >= NW * 32 && d <= NW * 256; }
 
-hipError_t launch_local_loss_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<0>(a, s); }
-hipError_t launch_readout_grad_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<1>(a, s); }
+hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s) {
+    return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
+}
+hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<EVAL, true>(a, 0, s); }
+hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_mode<RGRAD, false>(a, nmod, s);
+}
+hipError_t launch_bias_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_mode<BGRAD, false>(a, nmod, s);
+}
 
 }  // namespace solo

@@ -1,7 +1,8 @@
-// Bandwidth-light kernels around the two fused passes:
-//   - fold the RMSNorm gain into a copy of the readout (Wg = W diag(gain)),
+// Bandwidth-light kernels around the fused passes:
 //   - per-row inverse RMS of the hidden states,
-//   - fixed-order reductions for the module losses and the gain gradient.
+//   - the gain-scaled copy bf16(g_k * h_k) streamed by the matrix-core gradient passes,
+//   - fixed-order reductions for the module losses, the temperature gradients
+//     and the gain gradients.
 #include "solo_internal.h"
 
 namespace solo {
@@ -10,23 +11,6 @@ namespace {
 
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
 __device__ __forceinline__ float to_f32(float x) { return x; }
-template <typename E> __device__ __forceinline__ E from_f32(float x);
-template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
-template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
-
-// Wg[v][j] = W[v][j] * gain[j], rounded once to the storage type.
-// z_tv = <W_v, gain * n_t> = <Wg_v, n_t>, so the gain multiplies the readout
-// once per call instead of every row of every module.
-template <typename E>
-__global__ void k_prep_readout(const E* __restrict__ W, const E* __restrict__ gain, E* __restrict__ Wg,
-                               long long n, int d) {
-    long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    long long stride = (long long)gridDim.x * blockDim.x;
-    for (; i < n; i += stride) {
-        int j = (int)(i % d);
-        Wg[i] = from_f32<E>(to_f32(W[i]) * to_f32(gain[j]));
-    }
-}
 
 // rstd[row] = 1 / sqrt(mean_j h[row][j]^2 + eps); one wave per row.
 template <typename E>
@@ -47,11 +31,34 @@ __global__ void k_row_rstd(const E* __restrict__ h, float* __restrict__ rstd, lo
     }
 }
 
-// losses[k] = (1/T) sum_t rowloss[k][t], fixed order, fp64 accumulation.
-__global__ void k_module_loss(const float* __restrict__ rowloss, float* __restrict__ losses, int T) {
+// hg = bf16(h * g) elementwise, 8 elements per thread (d % 8 == 0): the same
+// product and rounding as the stationary-tile load of the local-loss pass.
+__global__ void k_prep_hg(const bf16* __restrict__ h, const bf16* __restrict__ gain, int g_stride,
+                          bf16* __restrict__ hg, int m0, long long per_mod, int T, int d) {
+    typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+    const long long n8 = per_mod / 8;
+    const int m = blockIdx.y;
+    const bf16* hm = h + (long long)(m0 + m) * per_mod;
+    const bf16* gm = gain + (long long)(m0 + m) * g_stride;
+    bf16* om = hg + (long long)m * per_mod;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (long long)gridDim.x * blockDim.x) {
+        const int j = (int)((i * 8) % d);
+        const bf16x8 hv = *(const bf16x8*)(hm + i * 8);
+        const bf16x8 gv = *(const bf16x8*)(gm + j);
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (bf16)((float)hv[e] * (float)gv[e]);
+        *(bf16x8*)(om + i * 8) = o;
+    }
+}
+
+// out[k] = scale * sum_t rows[k][t], fixed order, fp64 accumulation
+// (module losses: the per-token losses with scale 1/T; temperature gradients:
+// the per-token shares with scale 1).
+__global__ void k_module_sum(const float* __restrict__ rows, float* __restrict__ out, int T, double scale) {
     __shared__ double red[256];
     const int k = blockIdx.x;
-    const float* r = rowloss + (long long)k * T;
+    const float* r = rows + (long long)k * T;
     double acc = 0.0;
     for (int t = threadIdx.x; t < T; t += 256) acc += (double)r[t];
     red[threadIdx.x] = acc;
@@ -60,16 +67,18 @@ __global__ void k_module_loss(const float* __restrict__ rowloss, float* __restri
         if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
         __syncthreads();
     }
-    if (threadIdx.x == 0) losses[k] = (float)(red[0] / (double)T);
+    if (threadIdx.x == 0) out[k] = (float)(red[0] * scale);
 }
 
-// dgain[j] = sum over vocabulary tiles of part[tile][j], fixed order: a
-// block of 256 threads covers 32 columns; its 8 thread groups sum every
-// eighth tile, then the 8 group sums are added in group order.
+// dgain[slot][j] = sum over token tiles of part[slot][tile][j], fixed order:
+// a block of 256 threads covers 32 columns of one slot; its 8 thread groups
+// sum every eighth tile, then the 8 group sums are added in group order.
 __global__ void k_dgain_reduce(const float* __restrict__ part, float* __restrict__ dgain, int ntiles, int d) {
     __shared__ double red[8][32];
     const int jl = threadIdx.x & 31, grp = threadIdx.x >> 5;
     const int j = blockIdx.x * 32 + jl;
+    part += (long long)blockIdx.y * ntiles * d;
+    dgain += (long long)blockIdx.y * d;
     double acc = 0.0;
     if (j < d)
         for (int i = grp; i < ntiles; i += 8) acc += (double)part[(long long)i * d + j];
@@ -84,19 +93,6 @@ __global__ void k_dgain_reduce(const float* __restrict__ part, float* __restrict
 
 }  // namespace
 
-hipError_t launch_prep_readout(int dtype, const void* W, const void* gain, void* Wg, int V, int d, hipStream_t s) {
-    long long n = (long long)V * d;
-    long long blocks = (n + 255) / 256;
-    if (blocks > 65536) blocks = 65536;
-    if (dtype == 0)
-        hipLaunchKernelGGL(k_prep_readout<bf16>, dim3((unsigned)blocks), dim3(256), 0, s, (const bf16*)W,
-                           (const bf16*)gain, (bf16*)Wg, n, d);
-    else
-        hipLaunchKernelGGL(k_prep_readout<float>, dim3((unsigned)blocks), dim3(256), 0, s, (const float*)W,
-                           (const float*)gain, (float*)Wg, n, d);
-    return hipGetLastError();
-}
-
 hipError_t launch_row_rstd(int dtype, const void* h, float* rstd, long long rows, int d, float eps, hipStream_t s) {
     long long blocks = (rows + 3) / 4;
     if (dtype == 0)
@@ -106,13 +102,23 @@ hipError_t launch_row_rstd(int dtype, const void* h, float* rstd, long long rows
     return hipGetLastError();
 }
 
-hipError_t launch_module_loss(const float* rowloss, float* losses, int K, int T, hipStream_t s) {
-    hipLaunchKernelGGL(k_module_loss, dim3(K), dim3(256), 0, s, rowloss, losses, T);
+hipError_t launch_prep_hg(const bf16* h, const bf16* gain, int g_stride, bf16* hg, int m0, int nmod, int T, int d,
+                          hipStream_t s) {
+    const long long per_mod = (long long)T * d;
+    long long blocks = (per_mod / 8 + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_prep_hg, dim3((unsigned)blocks, (unsigned)nmod), dim3(256), 0, s, h, gain, g_stride, hg, m0,
+                       per_mod, T, d);
     return hipGetLastError();
 }
 
-hipError_t launch_dgain_reduce(const float* part, float* dgain, int ntiles, int d, hipStream_t s) {
-    hipLaunchKernelGGL(k_dgain_reduce, dim3((d + 31) / 32), dim3(256), 0, s, part, dgain, ntiles, d);
+hipError_t launch_module_sum(const float* rows, float* out, int K, int T, double scale, hipStream_t s) {
+    hipLaunchKernelGGL(k_module_sum, dim3(K), dim3(256), 0, s, rows, out, T, scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_dgain_reduce(const float* part, float* dgain, int slots, int ntiles, int d, hipStream_t s) {
+    hipLaunchKernelGGL(k_dgain_reduce, dim3((d + 31) / 32, slots), dim3(256), 0, s, part, dgain, ntiles, d);
     return hipGetLastError();
 }
 

@@ -1,14 +1,17 @@
-// Vector-ALU versions of the two fused passes (fp32 arithmetic on fp32 or
-// bf16 storage).  They serve the fp32 configuration, where the products must
-// be true fp32 products, and bf16 widths that the matrix-core kernels do not
-// tile.  Same structure as the matrix-core passes: a tile of stationary rows
-// stays in LDS/registers, the other operand streams in chunks, the T x V
-// logits are never written.
+// Vector-ALU versions of the fused passes (fp32 arithmetic on fp32 or bf16
+// storage).  They serve the fp32 configuration, where the products must be
+// true fp32 products, and bf16 widths that the matrix-core kernels do not
+// tile.  Same passes and notation as k_mfma.hip (z_tv = tau_k <R_kv, hhat_t> + b_kv,
+// hhat = g_k * r_t h_t): a tile of stationary rows stays in LDS, the other
+// operand streams in chunks, the T x V logits are never written.
 //
-//   local-loss pass: 8 rows t of h_k; online max / sum-exp over the readout
-//     rows; acc_t += sum_v exp(z_tv - m_t) Wg_v; RMSNorm backward at the end.
-//   readout-gradient pass: 8 readout rows v; delta from the stored lse;
-//     D_v += sum_t delta_tv r_t h_t; dW_v = gain * D_v; dgain partial W_v * D_v.
+//   local-loss pass: 8 rows t with hhat in LDS; online max / sum-exp over the
+//     readout rows; acc_t += sum_v exp(z_tv - m_t) R_kv; dhat, the RMSNorm
+//     backward and the tile's gain-gradient partial at the end.
+//   exit evaluation: the same without the second product, plus the top-1.
+//   readout-gradient pass: 8 readout rows v (times g_k); delta from the stored
+//     lse; D_v += sum_t delta_tv tau r_t h_t; dR_v = g_k * D_v; db_v = sum_t delta_tv.
+//   bias-gradient pass: the same without the second product.
 #include "solo_internal.h"
 
 namespace solo {
@@ -20,6 +23,8 @@ constexpr int YC = 64;         // streamed rows per chunk
 constexpr int NTHR = 256;
 constexpr int NQ = 16;         // columns per thread: j = tid + 256 q, d <= 4096
 
+enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
+
 __device__ __forceinline__ float ld(const float* p, long long i) { return p[i]; }
 __device__ __forceinline__ float ld(const bf16* p, long long i) { return (float)p[i]; }
 template <typename E> __device__ __forceinline__ void st(E* p, long long i, float v);
@@ -28,54 +33,63 @@ template <> __device__ __forceinline__ void st<bf16>(bf16* p, long long i, float
 
 template <typename E, int MODE>
 __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
+    constexpr bool LL = MODE == LOCAL || MODE == EVAL;   // X = hhat, Y = readout
+    constexpr bool PC = MODE == LOCAL || MODE == RGRAD;  // second product
     extern __shared__ __attribute__((aligned(16))) float sm[];
     const int d = a.d;
     float* xs = sm;                    // [RX][d] stationary rows (fp32)
     float* sS = xs + RX * d;           // [RX][YC] logits, then probabilities / deltas
     float* sc = sS + RX * YC;          // [RX] alpha, then 1/s
-    float* sy = sc + RX;               // [3][YC] per-streamed-row scalars (MODE 1)
+    float* sy = sc + RX;               // [3][YC] per-streamed-row scalars (readout-/bias-gradient passes)
     float* red = sy + 3 * YC;          // [RX][NTHR/64] reductions
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = tid >> 6;
     const int x0 = blockIdx.x * RX;
-    const int k = (MODE == 0) ? (int)blockIdx.y : a.K - 1;
+    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
     const long long modoff = (long long)k * a.T;
+    const float tau = a.tau ? a.tau[k] : 1.f;
     const E* hk = (const E*)a.h + modoff * d;
-    const E* Wg = (const E*)a.Wg;
-    const E* Y = (MODE == 0) ? Wg : hk;
-    const int nX = (MODE == 0) ? a.T : a.V;
-    const int nY = (MODE == 0) ? a.V : a.T;
+    const E* Rk = k == a.K - 1 ? (const E*)a.Wt : (const E*)a.Wh + (long long)k * a.wh_stride;
+    const E* gk = (const E*)a.gain + (long long)k * a.g_stride;
+    const float* bk = a.bias ? a.bias + (long long)k * a.V : nullptr;
+    const E* Y = LL ? Rk : hk;
+    const int nX = LL ? a.T : a.V;
+    const int nY = LL ? a.V : a.T;
 
-    // stationary tile: MODE 0 -> n_t = r_t h_t ; MODE 1 -> Wg_v
+    // stationary tile: LL -> hhat_t = g r_t h_t ; otherwise g * R_v
     for (int i = tid; i < RX * d; i += NTHR) {
         const int r = i / d, j = i - r * d;
         const int xg = x0 + r;
         float v = 0.f;
         if (xg < nX) {
-            if (MODE == 0) v = a.rstd[modoff + xg] * ld(hk, (long long)xg * d + j);
-            else v = ld(Wg, (long long)xg * d + j);
+            if (LL) v = ld(gk, j) * a.rstd[modoff + xg] * ld(hk, (long long)xg * d + j);
+            else v = ld(gk, j) * ld(Rk, (long long)xg * d + j);
         }
         xs[i] = v;
     }
 
-    float acc[RX][NQ];
+    float acc[PC ? RX : 1][NQ];
 #pragma unroll
-    for (int r = 0; r < RX; ++r)
+    for (int r = 0; r < (PC ? RX : 1); ++r)
 #pragma unroll
         for (int q = 0; q < NQ; ++q) acc[r][q] = 0.f;
 
-    // online softmax state (MODE 0): thread (r = tid/32) keeps row r's copy
-    const int sr = tid >> 5;          // row handled in the elementwise step
-    const int sq = tid & 31;          // columns sq and sq + 32 of the chunk
-    float m_run = -INFINITY, s_run = 0.f, zy = 0.f;
+    // elementwise step: thread (sr = tid/32, sq = tid%32) handles columns sq and sq + 32 of row sr
+    const int sr = tid >> 5;
+    const int sq = tid & 31;
+    float m_run = -INFINITY, s_run = 0.f, zy = 0.f, su = 0.f, uy = 0.f;
+    float best = -INFINITY;
+    int best_v = -1;
+    float dbp = 0.f;
     int own_tgt = -1;
-    if (MODE == 0 && x0 + sr < nX) own_tgt = a.targets[modoff + x0 + sr];
+    if (LL && x0 + sr < nX) own_tgt = a.targets[modoff + x0 + sr];
+    const float bx = (!LL && bk && x0 + sr < nX) ? bk[x0 + sr] : 0.f;
     __syncthreads();
 
     for (int y0 = 0; y0 < nY; y0 += YC) {
-        if (MODE == 1 && tid < YC) {
+        if (!LL && tid < YC) {
             const int yg = y0 + tid;
             const bool ok = yg < nY;
             sy[tid] = ok ? a.rstd[modoff + yg] : 0.f;
@@ -104,26 +118,41 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             }
             if (lane == 0) {
 #pragma unroll
-                for (int r = 0; r < RX; ++r) sS[r * YC + yy] = (yg < nY) ? part[r] : -INFINITY;
+                for (int r = 0; r < RX; ++r) sS[r * YC + yy] = part[r];
             }
         }
         __syncthreads();
 
-        // elementwise step: thread (sr, sq) handles columns sq, sq + 32 of row sr
-        if (MODE == 0) {
-            const float z0 = sS[sr * YC + sq], z1 = sS[sr * YC + sq + 32];
-            float cmax = fmaxf(z0, z1);
+        if (LL) {
+            float u[2], z[2];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                const int yg = y0 + sq + 32 * hh;
+                u[hh] = sS[sr * YC + sq + 32 * hh];
+                z[hh] = (yg < nY) ? tau * u[hh] + (bk ? bk[yg] : 0.f) : -INFINITY;
+                if (MODE == EVAL && z[hh] > best) {  // columns come in increasing order: ties keep the first
+                    best = z[hh];
+                    best_v = yg;
+                }
+                if (yg == own_tgt) {
+                    zy = z[hh];
+                    uy = u[hh];
+                }
+            }
+            float cmax = fmaxf(z[0], z[1]);
             for (int off = 16; off > 0; off >>= 1) cmax = fmaxf(cmax, __shfl_xor(cmax, off, 32));
             const float m_new = fmaxf(m_run, cmax);
             const float alpha = __expf(m_run - m_new);
             m_run = m_new;
-            const float p0 = (z0 == -INFINITY) ? 0.f : __expf(z0 - m_run);
-            const float p1 = (z1 == -INFINITY) ? 0.f : __expf(z1 - m_run);
-            float ps = p0 + p1;
-            for (int off = 16; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 32);
+            const float p0 = (z[0] == -INFINITY) ? 0.f : __expf(z[0] - m_run);
+            const float p1 = (z[1] == -INFINITY) ? 0.f : __expf(z[1] - m_run);
+            float ps = p0 + p1, pu = p0 * u[0] + p1 * u[1];
+            for (int off = 16; off > 0; off >>= 1) {
+                ps += __shfl_xor(ps, off, 32);
+                pu += __shfl_xor(pu, off, 32);
+            }
             s_run = s_run * alpha + ps;
-            if (y0 + sq == own_tgt) zy = z0;
-            if (y0 + sq + 32 == own_tgt) zy = z1;
+            su = su * alpha + pu;
             sS[sr * YC + sq] = p0;
             sS[sr * YC + sq + 32] = p1;
             if (sq == 0) sc[sr] = alpha;
@@ -136,74 +165,110 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                 float g = 0.f;
                 if (yg < nY && xg < nX) {
                     const float ry = sy[yy];
-                    const float p = __expf(sS[sr * YC + yy] * ry - sy[YC + yy]);
+                    const float p = __expf(tau * ry * sS[sr * YC + yy] + bx - sy[YC + yy]);
                     const int tg = __float_as_int(sy[2 * YC + yy]);
-                    g = (p - (tg == xg ? 1.f : 0.f)) * ry * a.inv_T;
+                    const float dl = p - (tg == xg ? 1.f : 0.f);
+                    dbp += dl;
+                    g = dl * ry * tau * a.inv_T;
                 }
                 sS[sr * YC + yy] = g;
             }
         }
         __syncthreads();
 
-        // second product: thread owns columns j = tid + 256 q of all RX rows
-        if (MODE == 0) {
+        if (PC) {
+            // second product: thread owns columns j = tid + 256 q of all RX rows
+            if (MODE == LOCAL) {
 #pragma unroll
-            for (int r = 0; r < RX; ++r) {
-                const float al = sc[r];
+                for (int r = 0; r < RX; ++r) {
+                    const float al = sc[r];
 #pragma unroll
-                for (int q = 0; q < NQ; ++q) acc[r][q] *= al;
+                    for (int q = 0; q < NQ; ++q) acc[r][q] *= al;
+                }
             }
-        }
-        const int yend = (nY - y0) < YC ? (nY - y0) : YC;
-        for (int yy = 0; yy < yend; ++yy) {
-            const E* yrow = Y + (long long)(y0 + yy) * d;
+            const int yend = (nY - y0) < YC ? (nY - y0) : YC;
+            for (int yy = 0; yy < yend; ++yy) {
+                const E* yrow = Y + (long long)(y0 + yy) * d;
 #pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-                const int j = tid + NTHR * q;
-                if (j < d) {
-                    const float yv = ld(yrow, j);
+                for (int q = 0; q < NQ; ++q) {
+                    const int j = tid + NTHR * q;
+                    if (j < d) {
+                        const float yv = ld(yrow, j);
 #pragma unroll
-                    for (int r = 0; r < RX; ++r) acc[r][q] = fmaf(sS[r * YC + yy], yv, acc[r][q]);
+                        for (int r = 0; r < RX; ++r) acc[PC ? r : 0][q] = fmaf(sS[r * YC + yy], yv, acc[PC ? r : 0][q]);
+                    }
                 }
             }
         }
         __syncthreads();
     }
 
-    if (MODE == 0) {
-        // finish rows: lse, row loss, 1/s (the target logit sits in one thread of the row group)
-        for (int off = 16; off > 0; off >>= 1) zy += __shfl_xor(zy, off, 32);
+    if (LL) {
+        // finish rows: lse, row loss, d loss / d tau, top-1; the target logit sits in one thread of the row group
+        for (int off = 16; off > 0; off >>= 1) {
+            zy += __shfl_xor(zy, off, 32);
+            uy += __shfl_xor(uy, off, 32);
+            if (MODE == EVAL) {
+                const float ob = __shfl_xor(best, off, 32);
+                const int ov = __shfl_xor(best_v, off, 32);
+                if (ob > best || (ob == best && (unsigned)ov < (unsigned)best_v)) {
+                    best = ob;
+                    best_v = ov;
+                }
+            }
+        }
         if (sq == 0) {
             const float lse = m_run + logf(s_run);
             const bool tok = own_tgt >= 0 && own_tgt < nY;
             if (x0 + sr < nX) {
-                a.lse[modoff + x0 + sr] = lse;
-                a.rowloss[modoff + x0 + sr] = tok ? lse - zy : __int_as_float(0x7fc00000);
+                const long long t = modoff + x0 + sr;
+                a.lse[t] = lse;
+                a.rowloss[t] = tok ? lse - zy : __int_as_float(0x7fc00000);
+                if (MODE == EVAL && a.top1) a.top1[t] = best_v;
+                if (MODE == LOCAL && a.rowdtau) a.rowdtau[t] = tok ? (su / s_run - uy) * a.inv_T : 0.f;
             }
             sc[sr] = 1.f / s_run;
         }
         __syncthreads();
-        // dn = (acc / s - Wg[y]) / T; c = mean(dn * n); dh = r (dn - c n)
+    }
+    if (MODE == LOCAL) {
+        // dhat = tau (acc / s - R_y) / T; dn = g dhat; c = mean(dn n); dh = r (dn - c n)
+        const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
+        float dgp[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) dgp[q] = 0.f;
         float cp[RX];
 #pragma unroll
         for (int r = 0; r < RX; ++r) {
             const int xg = x0 + r;
             const int tg = (xg < nX) ? a.targets[modoff + xg] : -1;
             const bool tok = tg >= 0 && tg < nY;
+            const float rx = (xg < nX) ? a.rstd[modoff + xg] : 0.f;
             cp[r] = 0.f;
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int j = tid + NTHR * q;
                 if (j < d) {
-                    const float wy = tok ? ld(Wg, (long long)tg * d + j) : 0.f;
-                    const float dn = (acc[r][q] * sc[r] - wy) * a.inv_T;
+                    const float wy = tok ? ld(Rk, (long long)tg * d + j) : 0.f;
+                    const float dhat = (acc[r][q] * sc[r] - wy) * tau * a.inv_T;
+                    const float n = (xg < nX) ? rx * ld(hk, (long long)xg * d + j) : 0.f;
+                    const float dn = ld(gk, j) * dhat;
                     acc[r][q] = dn;
-                    cp[r] = fmaf(dn, xs[r * d + j], cp[r]);
+                    cp[r] = fmaf(dn, n, cp[r]);
+                    dgp[q] = fmaf(dhat, n, dgp[q]);
                 }
             }
             float v = cp[r];
             for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
             if (lane == 0) red[r * (NTHR / 64) + wv] = v;
+        }
+        if (want_dg) {
+            float* part = a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const int j = tid + NTHR * q;
+                if (j < d) part[j] = dgp[q];
+            }
         }
         __syncthreads();
 #pragma unroll
@@ -218,50 +283,58 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int j = tid + NTHR * q;
-                if (j < d) st<E>(out, j, rx * (acc[r][q] - cmean * xs[r * d + j]));
+                if (j < d) st<E>(out, j, rx * (acc[r][q] - cmean * rx * ld(hk, (long long)xg * d + j)));
             }
         }
-    } else {
-        const E* W = (const E*)a.W;
-        const E* gain = (const E*)a.gain;
-        float* dgp = a.dgain_part + (long long)blockIdx.x * d;
+    }
+    if (!LL) {
+        // bias gradient of readout row sr: sum over the 32 threads of the row group
+        for (int off = 16; off > 0; off >>= 1) dbp += __shfl_xor(dbp, off, 32);
+        if (a.dbias && sq == 0 && x0 + sr < nX) a.dbias[(long long)k * a.V + x0 + sr] = dbp * a.inv_T;
+    }
+    if (MODE == RGRAD) {
+        float* dR = (k == a.K - 1) ? a.dWt : a.dWh + (long long)k * a.V * d;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int j = tid + NTHR * q;
             if (j >= d) continue;
-            const float gj = ld(gain, j);
-            float pr = 0.f;
+            const float gj = ld(gk, j);
 #pragma unroll
             for (int r = 0; r < RX; ++r) {
                 const int v = x0 + r;
-                if (v < nX) {
-                    a.dW[(long long)v * d + j] = gj * acc[r][q];
-                    pr = fmaf(ld(W, (long long)v * d + j), acc[r][q], pr);
-                }
+                if (v < nX) dR[(long long)v * d + j] = gj * acc[PC ? r : 0][q];
             }
-            dgp[j] = pr;
         }
     }
 }
 
 template <typename E, int MODE>
-hipError_t launch_t(const FusedArgs& a, hipStream_t s) {
+hipError_t launch_t(const FusedArgs& a, int nmod, hipStream_t s) {
     const size_t lds = sizeof(float) * ((size_t)RX * a.d + RX * YC + RX + 3 * YC + RX * (NTHR / 64));
     hipError_t e = hipFuncSetAttribute((const void*)k_fused_valu<E, MODE>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds);
     if (e != hipSuccess) return e;
-    dim3 grid = (MODE == 0) ? dim3((unsigned)((a.T + RX - 1) / RX), (unsigned)a.K) : dim3((unsigned)((a.V + RX - 1) / RX));
+    const bool ll = MODE == LOCAL || MODE == EVAL;
+    dim3 grid = ll ? dim3((unsigned)((a.T + RX - 1) / RX), (unsigned)a.K)
+                   : dim3((unsigned)((a.V + RX - 1) / RX), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused_valu<E, MODE>), grid, dim3(NTHR), lds, s, a);
     return hipGetLastError();
 }
 
+template <int MODE>
+hipError_t launch_dt(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
+    return dtype == 0 ? launch_t<bf16, MODE>(a, nmod, s) : launch_t<float, MODE>(a, nmod, s);
+}
+
 }  // namespace
 
-hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s) {
-    return dtype == 0 ? launch_t<bf16, 0>(a, s) : launch_t<float, 0>(a, s);
+hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s) { return launch_dt<LOCAL>(dtype, a, 0, s); }
+hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, hipStream_t s) { return launch_dt<EVAL>(dtype, a, 0, s); }
+hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_dt<RGRAD>(dtype, a, nmod, s);
 }
-hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, hipStream_t s) {
-    return dtype == 0 ? launch_t<bf16, 1>(a, s) : launch_t<float, 1>(a, s);
+hipError_t launch_bias_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_dt<BGRAD>(dtype, a, nmod, s);
 }
 
 }  // namespace solo

@@ -57,6 +57,21 @@ __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, unsigned lds_base,
         : "memory");
 }
 
+// Same for 4 bytes per lane: lane l's dword lands at lds_base + 4 l.
+__device__ __forceinline__ void buffer_load_lds4(i32x4 rsrc, unsigned lds_base, int voffset) {
+    unsigned saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dword %2, %3, 0 offen lds\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voffset), "s"(rsrc)
+        : "memory");
+}
+
 // All-lane reductions over each 16-lane row of the wave (DPP: quad
 // permutations, then rotations by 4 and 8 inside the row).
 template <int CTRL>

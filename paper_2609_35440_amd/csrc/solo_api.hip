@@ -12,12 +12,6 @@ constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-struct Layout {
-    size_t wg, rstd, lse, rowloss, rowrec, dgp, total;
-    int ntiles;
-    bool mfma;
-};
-
 bool shape_ok(int K, int T, int d, int V) {
     if (K < 1 || T < 1 || V < 1) return false;
     if (d < 8 || d % 8 != 0 || d > 4096) return false;
@@ -26,31 +20,238 @@ bool shape_ok(int K, int T, int d, int V) {
     return true;
 }
 
-bool make_layout(int K, int T, int d, int V, int dtype, int fdw, Layout* L) {
-    if (dtype != SOLO_BF16 && dtype != SOLO_F32) return false;
-    if (!shape_ok(K, T, d, V)) return false;
-    const size_t elem = dtype == SOLO_BF16 ? 2 : 4;
-    L->mfma = solo::mfma_supported(dtype, d);
-    const int vtile = L->mfma ? solo::kMfmaRows : solo::kValuRows;
+bool flag_ok(int f) { return f == 0 || f == 1; }
+
+// What one call launches, and where its workspace pieces sit.
+struct Plan {
+    bool mfma = false;
+    bool eval = false;
+    bool ext = false;          // local-loss variant with biases and temperature-gradient sums
+    int dg_mode = 0;           // 0 none, 1 terminal only, 2 every module
+    int slots = 0;             // gain-gradient partial slots
+    int ntiles = 0;            // token tiles of the local-loss pass
+    int rg_lo = 0, rg_hi = 0;  // modules of the readout-gradient pass
+    int bg_lo = 0, bg_hi = 0;  // modules of the bias-gradient pass
+    int hg_lo = 0, hg_hi = 0;  // modules whose gain-scaled copy the matrix-core gradient passes stream
+    size_t rstd = 0, lse = 0, rowloss = 0, rowrec = 0, rowdtau = 0, dgp = 0, hg = 0, total = 0;
+};
+
+// Sizes, dtype and flags only (no pointer is dereferenced).
+bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
+    if (a.dtype != SOLO_BF16 && a.dtype != SOLO_F32) return false;
+    if (!shape_ok(a.K, a.T, a.d, a.V)) return false;
+    if (!flag_ok(a.gain_per_module) || !flag_ok(a.readout_per_head) || !flag_ok(a.final_module_dW) ||
+        !flag_ok(a.heads_train_readout))
+        return false;
+    const int K = a.K, T = a.T, d = a.d;
+    P->mfma = solo::mfma_supported(a.dtype, d);
+    P->eval = eval;
+    const size_t kt = (size_t)K * T;
     size_t off = 0;
-    L->wg = off;
-    off = align_up(off + (size_t)V * d * elem);
-    L->rstd = off;
-    off = align_up(off + (size_t)K * T * 4);
-    L->lse = off;
-    off = align_up(off + (size_t)K * T * 4);
-    L->rowloss = off;
-    off = align_up(off + (size_t)K * T * 4);
-    L->rowrec = off;
-    off = align_up(off + (fdw ? (size_t)T * 16 : 0));
-    L->ntiles = fdw ? (V + vtile - 1) / vtile : 0;
-    L->dgp = off;
-    off = align_up(off + (size_t)L->ntiles * d * 4);
-    L->total = off;
+    P->rstd = off;
+    off = align_up(off + kt * 4);
+    P->lse = off;
+    off = align_up(off + kt * 4);
+    P->rowloss = off;
+    off = align_up(off + kt * 4);
+    if (eval) {
+        P->total = off;
+        return true;
+    }
+    const bool priv = a.heads_train_readout && K > 1;
+    const bool fdw = a.final_module_dW;
+    // readout-gradient modules: the terminal if its dW is asked for, the heads under PRIV
+    P->rg_lo = priv ? 0 : K - 1;
+    P->rg_hi = fdw ? K : (priv ? K - 1 : K - 1);
+    if (!fdw && !priv) P->rg_lo = P->rg_hi = 0;
+    // bias-gradient modules: every other module, if the bias gradient is asked for
+    if (a.dbias) {
+        if (P->rg_hi == P->rg_lo) {
+            P->bg_lo = 0;
+            P->bg_hi = K;
+        } else if (P->rg_lo == 0 && P->rg_hi == K) {
+            P->bg_lo = P->bg_hi = 0;
+        } else if (P->rg_lo == 0) {
+            P->bg_lo = K - 1;
+            P->bg_hi = K;
+        } else {
+            P->bg_lo = 0;
+            P->bg_hi = K - 1;
+        }
+    }
+    P->ext = a.bias != nullptr || a.dtau != nullptr;
+    P->dg_mode = a.gain_per_module ? 2 : (fdw ? 1 : 0);
+    P->slots = P->dg_mode == 2 ? K : (P->dg_mode == 1 ? 1 : 0);
+    const int rows = P->mfma ? solo::kMfmaRows : solo::kValuRows;
+    P->ntiles = (T + rows - 1) / rows;
+    const bool second = P->rg_hi > P->rg_lo || P->bg_hi > P->bg_lo;
+    if (P->mfma && second) {
+        // the two ranges are disjoint parts of [0, K): their union is one range
+        const bool rg = P->rg_hi > P->rg_lo, bg = P->bg_hi > P->bg_lo;
+        P->hg_lo = rg && bg ? (P->rg_lo < P->bg_lo ? P->rg_lo : P->bg_lo) : (rg ? P->rg_lo : P->bg_lo);
+        P->hg_hi = rg && bg ? (P->rg_hi > P->bg_hi ? P->rg_hi : P->bg_hi) : (rg ? P->rg_hi : P->bg_hi);
+    }
+    P->rowrec = off;
+    off = align_up(off + ((P->mfma && second) ? kt * 16 : 0));
+    P->hg = off;
+    off = align_up(off + (size_t)(P->hg_hi - P->hg_lo) * T * d * 2);
+    P->rowdtau = off;
+    off = align_up(off + (a.dtau ? kt * 4 : 0));
+    P->dgp = off;
+    off = align_up(off + (size_t)P->slots * P->ntiles * d * 4);
+    P->total = off;
     return true;
 }
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+bool aligned_or_null(const void* p, uintptr_t a) { return !p || aligned(p, a); }
+
+int check(const solo_readout_args& a, bool eval, Plan* P) {
+    if (a.dtype != SOLO_BF16 && a.dtype != SOLO_F32) return SOLO_ERR_DTYPE;
+    if (!shape_ok(a.K, a.T, a.d, a.V)) return SOLO_ERR_SHAPE;
+    if (!std::isfinite(a.eps) || a.eps < 0.f) return SOLO_ERR_ARG;
+    if (!flag_ok(a.gain_per_module) || !flag_ok(a.readout_per_head) || !flag_ok(a.final_module_dW) ||
+        !flag_ok(a.heads_train_readout))
+        return SOLO_ERR_ARG;
+    if (a.readout_per_head && !a.Wbar) return SOLO_ERR_ARG;
+    if (a.heads_train_readout && !a.readout_per_head) return SOLO_ERR_ARG;
+    if (!a.h || !a.gain || !a.W || !a.targets || !a.losses || !a.workspace) return SOLO_ERR_NULL;
+    if (!eval) {
+        if (!a.dh) return SOLO_ERR_NULL;
+        if (a.final_module_dW && !a.dW) return SOLO_ERR_NULL;
+        if (a.heads_train_readout && a.K > 1 && !a.dWbar) return SOLO_ERR_NULL;
+        if ((a.gain_per_module || a.final_module_dW) && !a.dgain) return SOLO_ERR_NULL;
+    }
+    if (!aligned(a.h, 16) || !aligned(a.gain, 16) || !aligned(a.W, 16) || !aligned_or_null(a.Wbar, 16) ||
+        !aligned(a.targets, 4) || !aligned(a.losses, 4) || !aligned_or_null(a.row_loss, 4) ||
+        !aligned_or_null(a.tau, 4) || !aligned_or_null(a.bias, 4) || !aligned(a.workspace, kAlign))
+        return SOLO_ERR_ALIGN;
+    if (eval) {
+        if (!aligned_or_null(a.top1, 4)) return SOLO_ERR_ALIGN;
+    } else {
+        if (!aligned(a.dh, 16) || !aligned_or_null(a.dtau, 4) || !aligned_or_null(a.dbias, 4))
+            return SOLO_ERR_ALIGN;
+        if (a.final_module_dW && !aligned(a.dW, 16)) return SOLO_ERR_ALIGN;
+        if (a.heads_train_readout && a.K > 1 && !aligned(a.dWbar, 16)) return SOLO_ERR_ALIGN;
+        if ((a.gain_per_module || a.final_module_dW) && !aligned(a.dgain, 4)) return SOLO_ERR_ALIGN;
+    }
+    if (!make_plan(a, eval, P)) return SOLO_ERR_SHAPE;
+    if (a.workspace_bytes < P->total) return SOLO_ERR_WORKSPACE;
+    return SOLO_OK;
+}
+
+int run(const solo_readout_args& x, bool eval) {
+    Plan P;
+    const int st = check(x, eval, &P);
+    if (st != SOLO_OK) return st;
+    const int K = x.K, T = x.T, d = x.d, V = x.V;
+    hipStream_t s = (hipStream_t)x.hip_stream;
+    char* ws = (char*)x.workspace;
+    const size_t elem = x.dtype == SOLO_BF16 ? 2 : 4;
+
+    solo::FusedArgs a = {};
+    a.K = K;
+    a.T = T;
+    a.d = d;
+    a.V = V;
+    a.m0 = 0;
+    a.inv_T = (float)(1.0 / (double)T);
+    a.h = x.h;
+    a.Wt = x.W;
+    // heads: W itself, one shared matrix, or one per head
+    a.Wh = x.Wbar ? x.Wbar : x.W;
+    a.wh_stride = (x.Wbar && x.readout_per_head) ? (long long)V * d : 0;
+    a.hg = ws + P.hg;
+    a.hg_m0 = P.hg_lo;
+    a.gain = x.gain;
+    a.g_stride = x.gain_per_module ? d : 0;
+    a.tau = x.tau;
+    a.bias = x.bias;
+    a.targets = x.targets;
+    a.rstd = (const float*)(ws + P.rstd);
+    a.lse = (float*)(ws + P.lse);
+    a.rowloss = x.row_loss ? x.row_loss : (float*)(ws + P.rowloss);
+    a.rowrec = (!eval && P.mfma && (P.rg_hi > P.rg_lo || P.bg_hi > P.bg_lo)) ? (float*)(ws + P.rowrec) : nullptr;
+    a.rowdtau = (!eval && x.dtau) ? (float*)(ws + P.rowdtau) : nullptr;
+    a.top1 = eval ? x.top1 : nullptr;
+    a.dh = eval ? nullptr : x.dh;
+    a.dgain_part = P.slots ? (float*)(ws + P.dgp) : nullptr;
+    a.dg_mode = eval ? 0 : P.dg_mode;
+    a.dWt = (!eval && x.final_module_dW) ? x.dW : nullptr;
+    a.dWh = (!eval && x.heads_train_readout) ? x.dWbar : nullptr;
+    a.dbias = eval ? nullptr : x.dbias;
+    (void)elem;
+
+    auto mark = [&](int stage) -> bool {
+        if (!x.stage_events || !x.stage_events[stage]) return true;
+        return hipEventRecord((hipEvent_t)x.stage_events[stage], s) == hipSuccess;
+    };
+    const int dt = x.dtype;
+    if (solo::launch_row_rstd(dt, x.h, (float*)(ws + P.rstd), (long long)K * T, d, x.eps, s) != hipSuccess ||
+        !mark(0))
+        return SOLO_ERR_HIP;
+    hipError_t e;
+    if (eval)
+        e = P.mfma ? solo::launch_exit_eval_mfma(a, s) : solo::launch_exit_eval_valu(dt, a, s);
+    else
+        e = P.mfma ? solo::launch_local_loss_mfma(a, P.ext, s) : solo::launch_local_loss_valu(dt, a, s);
+    if (e != hipSuccess || !mark(1)) return SOLO_ERR_HIP;
+    if (solo::launch_module_sum(a.rowloss, x.losses, K, T, 1.0 / (double)T, s) != hipSuccess) return SOLO_ERR_HIP;
+    if (a.rowdtau && solo::launch_module_sum(a.rowdtau, x.dtau, K, T, 1.0, s) != hipSuccess) return SOLO_ERR_HIP;
+    if (!mark(2)) return SOLO_ERR_HIP;
+    if (!eval && P.hg_hi > P.hg_lo &&
+        solo::launch_prep_hg((const solo::bf16*)x.h, (const solo::bf16*)x.gain, a.g_stride, (solo::bf16*)(ws + P.hg),
+                             P.hg_lo, P.hg_hi - P.hg_lo, T, d, s) != hipSuccess)
+        return SOLO_ERR_HIP;
+    if (!eval && P.rg_hi > P.rg_lo) {
+        a.m0 = P.rg_lo;
+        const int n = P.rg_hi - P.rg_lo;
+        e = P.mfma ? solo::launch_readout_grad_mfma(a, n, s) : solo::launch_readout_grad_valu(dt, a, n, s);
+        if (e != hipSuccess) return SOLO_ERR_HIP;
+    }
+    if (!mark(3)) return SOLO_ERR_HIP;
+    if (!eval && P.bg_hi > P.bg_lo) {
+        a.m0 = P.bg_lo;
+        const int n = P.bg_hi - P.bg_lo;
+        e = P.mfma ? solo::launch_bias_grad_mfma(a, n, s) : solo::launch_bias_grad_valu(dt, a, n, s);
+        if (e != hipSuccess) return SOLO_ERR_HIP;
+    }
+    if (!mark(4)) return SOLO_ERR_HIP;
+    if (!eval && P.slots) {
+        if (solo::launch_dgain_reduce(a.dgain_part, x.dgain, P.slots, P.ntiles, d, s) != hipSuccess)
+            return SOLO_ERR_HIP;
+    }
+    if (!mark(5)) return SOLO_ERR_HIP;
+    return SOLO_OK;
+}
+
+solo_readout_args headline(int K, int T, int d, int V, int dtype, float eps, const void* h, const void* gain,
+                           const void* W, const int32_t* targets, int final_module_dW, float* losses,
+                           float* row_loss, void* dh, float* dW, float* dgain, void* workspace,
+                           size_t workspace_bytes, void* hip_stream, void* const* stage_events) {
+    solo_readout_args a = {};
+    a.K = K;
+    a.T = T;
+    a.d = d;
+    a.V = V;
+    a.dtype = dtype;
+    a.eps = eps;
+    a.h = h;
+    a.gain = gain;
+    a.W = W;
+    a.targets = targets;
+    a.final_module_dW = final_module_dW;
+    a.losses = losses;
+    a.row_loss = row_loss;
+    a.dh = dh;
+    a.dW = dW;
+    a.dgain = dgain;
+    a.workspace = workspace;
+    a.workspace_bytes = workspace_bytes;
+    a.hip_stream = hip_stream;
+    a.stage_events = stage_events;
+    return a;
+}
 
 }  // namespace
 
@@ -66,23 +267,24 @@ const char* solo_status_string(int status) {
         case SOLO_ERR_DTYPE: return "unknown dtype";
         case SOLO_ERR_ALIGN: return "misaligned pointer";
         case SOLO_ERR_WORKSPACE: return "workspace too small";
-        case SOLO_ERR_ARG: return "invalid argument (eps must be finite and >= 0; final_module_dW must be 0 or 1)";
+        case SOLO_ERR_ARG:
+            return "invalid argument (eps must be finite and >= 0; flags must be 0 or 1; readout_per_head needs "
+                   "Wbar; heads_train_readout needs readout_per_head)";
         case SOLO_ERR_HIP: return "HIP launch failed";
         default: return "unknown status";
     }
 }
 
 size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int final_module_dW) {
-    if (final_module_dW != 0 && final_module_dW != 1) return 0;
-    Layout L;
-    if (!make_layout(K, T, d, V, dtype, final_module_dW, &L)) return 0;
-    return L.total;
+    const solo_readout_args a = headline(K, T, d, V, dtype, 0.f, nullptr, nullptr, nullptr, nullptr, final_module_dW,
+                                         nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr);
+    Plan P;
+    return make_plan(a, false, &P) ? P.total : 0;
 }
 
 const char* solo_readout_kernel_family(int K, int T, int d, int V, int dtype) {
-    Layout L;
-    if (!make_layout(K, T, d, V, dtype, 0, &L)) return "invalid";
-    return L.mfma ? "mfma" : "valu";
+    if ((dtype != SOLO_BF16 && dtype != SOLO_F32) || !shape_ok(K, T, d, V)) return "invalid";
+    return solo::mfma_supported(dtype, d) ? "mfma" : "valu";
 }
 
 int solo_readout_fwd_bwd(int K, int T, int d, int V, int dtype, float eps, const void* h, const void* gain,
@@ -99,56 +301,30 @@ int solo_readout_fwd_bwd_profiled(int K, int T, int d, int V, int dtype, float e
                                   size_t workspace_bytes, void* hip_stream, void* const* stage_events) {
     if (dtype != SOLO_BF16 && dtype != SOLO_F32) return SOLO_ERR_DTYPE;
     if (!shape_ok(K, T, d, V)) return SOLO_ERR_SHAPE;
-    if (!std::isfinite(eps) || eps < 0.f) return SOLO_ERR_ARG;
-    if (final_module_dW != 0 && final_module_dW != 1) return SOLO_ERR_ARG;
-    if (!h || !gain || !W || !targets || !losses || !dh || !workspace) return SOLO_ERR_NULL;
-    if (final_module_dW && (!dW || !dgain)) return SOLO_ERR_NULL;
-    if (!aligned(h, 16) || !aligned(gain, 16) || !aligned(W, 16) || !aligned(dh, 16) || !aligned(targets, 4) ||
-        !aligned(losses, 4) || (row_loss && !aligned(row_loss, 4)) || !aligned(workspace, kAlign))
-        return SOLO_ERR_ALIGN;
-    if (final_module_dW && (!aligned(dW, 16) || !aligned(dgain, 4))) return SOLO_ERR_ALIGN;
-    Layout L;
-    if (!make_layout(K, T, d, V, dtype, final_module_dW, &L)) return SOLO_ERR_SHAPE;
-    if (workspace_bytes < L.total) return SOLO_ERR_WORKSPACE;
+    const solo_readout_args a = headline(K, T, d, V, dtype, eps, h, gain, W, targets, final_module_dW, losses,
+                                         row_loss, dh, dW, dgain, workspace, workspace_bytes, hip_stream,
+                                         stage_events);
+    return run(a, false);
+}
 
-    hipStream_t s = (hipStream_t)hip_stream;
-    char* ws = (char*)workspace;
-    solo::FusedArgs a;
-    a.K = K;
-    a.T = T;
-    a.d = d;
-    a.V = V;
-    a.inv_T = (float)(1.0 / (double)T);
-    a.h = h;
-    a.Wg = ws + L.wg;
-    a.W = W;
-    a.gain = gain;
-    a.targets = targets;
-    a.rstd = (const float*)(ws + L.rstd);
-    a.lse = (float*)(ws + L.lse);
-    a.rowloss = row_loss ? row_loss : (float*)(ws + L.rowloss);
-    a.rowrec = final_module_dW ? (float*)(ws + L.rowrec) : nullptr;
-    a.dh = dh;
-    a.dW = final_module_dW ? dW : nullptr;
-    a.dgain_part = (float*)(ws + L.dgp);
+size_t solo_readout_general_workspace_size(const solo_readout_args* args) {
+    Plan P;
+    return (args && make_plan(*args, false, &P)) ? P.total : 0;
+}
 
-    auto mark = [&](int stage) -> bool {
-        if (!stage_events || !stage_events[stage]) return true;
-        return hipEventRecord((hipEvent_t)stage_events[stage], s) == hipSuccess;
-    };
-    if (solo::launch_prep_readout(dtype, W, gain, ws + L.wg, V, d, s) != hipSuccess || !mark(0)) return SOLO_ERR_HIP;
-    if (solo::launch_row_rstd(dtype, h, (float*)(ws + L.rstd), (long long)K * T, d, eps, s) != hipSuccess || !mark(1))
-        return SOLO_ERR_HIP;
-    hipError_t e = L.mfma ? solo::launch_local_loss_mfma(a, s) : solo::launch_local_loss_valu(dtype, a, s);
-    if (e != hipSuccess || !mark(2)) return SOLO_ERR_HIP;
-    if (solo::launch_module_loss(a.rowloss, losses, K, T, s) != hipSuccess || !mark(3)) return SOLO_ERR_HIP;
-    if (final_module_dW) {
-        e = L.mfma ? solo::launch_readout_grad_mfma(a, s) : solo::launch_readout_grad_valu(dtype, a, s);
-        if (e != hipSuccess || !mark(4)) return SOLO_ERR_HIP;
-        if (solo::launch_dgain_reduce(a.dgain_part, dgain, L.ntiles, d, s) != hipSuccess || !mark(5))
-            return SOLO_ERR_HIP;
-    }
-    return SOLO_OK;
+int solo_readout_general(const solo_readout_args* args) {
+    if (!args) return SOLO_ERR_NULL;
+    return run(*args, false);
+}
+
+size_t solo_readout_exit_eval_workspace_size(const solo_readout_args* args) {
+    Plan P;
+    return (args && make_plan(*args, true, &P)) ? P.total : 0;
+}
+
+int solo_readout_exit_eval(const solo_readout_args* args) {
+    if (!args) return SOLO_ERR_NULL;
+    return run(*args, true);
 }
 
 }  // extern "C"

@@ -11,23 +11,42 @@ typedef __bf16 bf16;
 
 // Everything one fused pass needs.  The fused kernels keep a tile of
 // "stationary" rows (X) on chip and stream "streamed" rows (Y) in chunks:
-//   local-loss pass:    X = h of module k (rows t), Y = readout rows (v)
-//   readout-grad pass:  X = readout rows (v),       Y = h of the final module (rows t)
+//   local-loss pass:      X = g_k * h_k (rows t),     Y = readout of module k (rows v)
+//   exit evaluation:      same, forward only
+//   readout-grad pass:    X = readout_k (rows v),       Y = g_k * h_k (rows t)
+//   bias-grad pass:       same, without the second product
+// In the matrix-core passes both products see the same rounded operands
+// bf16(g_k * h_k) and R_k: the local-loss pass rounds g_k * h_k while it loads
+// its stationary tile, and the readout-/bias-gradient passes stream a copy
+// that a small kernel wrote with the same rounding (so their recomputed
+// logits match the stored log-sum-exp).
 struct FusedArgs {
     int K, T, d, V;
+    int m0;               // readout-/bias-gradient passes: module of grid row 0 (module = m0 + blockIdx.y)
     float inv_T;
     const void* h;        // [K][T][d] elem
-    const void* Wg;       // [V][d] elem: readout with the gain folded in (workspace)
-    const void* W;        // [V][d] elem: readout as given (dgain epilogue)
-    const void* gain;     // [d] elem
+    const void* Wt;       // [V][d] elem: readout of module K-1 (the terminal)
+    const void* Wh;       // elem: readout of module k < K-1 at Wh + k * wh_stride
+    long long wh_stride;  // elements; 0 when every head reads the same matrix
+    const void* hg;       // [..][T][d] bf16: bf16(g_k * h_k) of modules hg_m0.. (matrix-core gradient passes)
+    int hg_m0;
+    const void* gain;     // elem: gain of module k at gain + k * g_stride
+    int g_stride;         // 0 (one gain) or d (one per module)
+    const float* tau;     // [K] or null (temperature 1)
+    const float* bias;    // [K][V] or null (no bias)
     const int32_t* targets;  // [K][T]
     const float* rstd;    // [K][T] 1/sqrt(mean h^2 + eps)
-    float* lse;           // [K][T] log-sum-exp (written by the local-loss pass)
-    float* rowrec;        // [T][4] final module: {lse log2 e, rstd log2 e, target bits, rstd / T} per token
+    float* lse;           // [K][T] log-sum-exp of the logits (written by the local-loss pass)
+    float* rowrec;        // [K][T][4] or null: {lse log2 e, r tau log2 e, target bits, r tau / T} per token
     float* rowloss;       // [K][T] per-token cross-entropy
+    float* rowdtau;       // [K][T] or null: per-token share of d loss / d tau
+    int32_t* top1;        // [K][T] or null: exit evaluation, argmax of the logits (lowest index on ties)
     void* dh;             // [K][T][d] elem
-    float* dW;            // [V][d]
-    float* dgain_part;    // [ceil(V / vtile)][d] per-vocab-tile partial sums of W * D
+    float* dgain_part;    // [slots][gridDim.x][d]: per-tile partial sums of dhhat * n
+    int dg_mode;          // 0: no gain gradient; 1: module K-1 only (slot 0); 2: every module (slot k)
+    float* dWt;           // [V][d] or null: d loss_{K-1} / d W
+    float* dWh;           // [K-1][V][d] or null: d loss_k / d readout_k of the heads
+    float* dbias;         // [K][V] or null: d loss_k / d b_k
 };
 
 // Tile sizes of the two kernel families (the workspace depends on them).
@@ -35,16 +54,25 @@ constexpr int kMfmaRows = 32;      // stationary rows per workgroup (matrix-core
 constexpr int kValuRows = 8;       // stationary rows per workgroup (vector-ALU kernels)
 
 // small kernels (k_small.hip)
-hipError_t launch_prep_readout(int dtype, const void* W, const void* gain, void* Wg, int V, int d, hipStream_t s);
 hipError_t launch_row_rstd(int dtype, const void* h, float* rstd, long long rows, int d, float eps, hipStream_t s);
-hipError_t launch_module_loss(const float* rowloss, float* losses, int K, int T, hipStream_t s);
-hipError_t launch_dgain_reduce(const float* part, float* dgain, int ntiles, int d, hipStream_t s);
+// hg[m][t][j] = bf16(h[m0 + m][t][j] * gain[(m0 + m) g_stride + j]) for m in [0, nmod)
+hipError_t launch_prep_hg(const bf16* h, const bf16* gain, int g_stride, bf16* hg, int m0, int nmod, int T, int d,
+                          hipStream_t s);
+// out[k] = scale * sum_t rows[k][t], fixed order
+hipError_t launch_module_sum(const float* rows, float* out, int K, int T, double scale, hipStream_t s);
+// dgain[slot][j] = sum over tiles of part[slot][tile][j], fixed order
+hipError_t launch_dgain_reduce(const float* part, float* dgain, int slots, int ntiles, int d, hipStream_t s);
 
-// fused passes
+// fused passes; `ext` selects the local-loss variant with bias and temperature
+// gradient, `nmod` is the number of modules of a readout-/bias-gradient launch
 bool mfma_supported(int dtype, int d);
-hipError_t launch_local_loss_mfma(const FusedArgs& a, hipStream_t s);
-hipError_t launch_readout_grad_mfma(const FusedArgs& a, hipStream_t s);
+hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s);
+hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s);
+hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
+hipError_t launch_bias_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s);
-hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, hipStream_t s);
+hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, hipStream_t s);
+hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
+hipError_t launch_bias_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
 
 }  // namespace solo

@@ -26,6 +26,7 @@ __all__ = [
     "round_bf16",
     "zipf_targets",
     "make_inputs",
+    "make_extras",
 ]
 
 
@@ -76,6 +77,7 @@ CONFIGS: Dict[str, Config] = {
 
 # tensor ids inside one (seed, config) stream family
 _H, _W, _GAIN, _TARGETS, _HOT = 0, 1, 2, 3, 4
+_GAIN_K, _WBAR, _TAU, _BIAS = 5, 6, 7, 8
 
 
 def _rng(seed: int, config_id: int, tensor_id: int) -> np.random.Generator:
@@ -190,4 +192,42 @@ def make_inputs(cfg: Config | str, seed: int = 0, *, K: Optional[int] = None, T:
         out["W"] = np.ascontiguousarray(W)
     else:
         raise ValueError(f"unknown dtype {cfg.dtype!r}")
+    return out
+
+
+def make_extras(x: dict, seed: int = 0, *, per_module_gain: bool = False, wbar: str = "none",
+                tau: bool = False, bias: bool = False) -> dict:
+    """Extra inputs of the general call for the workload ``x`` (from make_inputs).
+
+    ``per_module_gain``: ``gain`` becomes [K, d], 1 + N(0, gain_sigma^2) per module.
+    ``wbar``: "none" (the heads read W), "shared" (one [V, d] matrix, drawn like W:
+    an earlier step's copy or a shared random readout) or "per_head" ([K-1, V, d]).
+    ``tau``: temperatures [K] uniform on [0.5, 2) (learned logit scales), fp32.
+    ``bias``: biases [K, V], N(0, 0.5^2), fp32.
+    Returns a dict with the same keys as make_inputs (``gain``, ``gain_bits``
+    replaced when per-module) plus ``Wbar`` (and ``Wbar_bits``), ``tau``, ``bias``
+    (None when absent).  Tensor values are exactly representable in the dtype.
+    """
+    cfg = x["cfg"]
+    K, d, V = cfg.K, cfg.d, cfg.V
+    out = dict(x)
+    bf = cfg.dtype == "bf16"
+
+    def stored(a):
+        return (bf16_bits(a), bf16_from_bits(bf16_bits(a))) if bf else (None, np.ascontiguousarray(a))
+
+    if per_module_gain:
+        g = np.float32(1.0) + _normal_f32(_rng(seed, cfg.config_id, _GAIN_K), (K, d), cfg.gain_sigma)
+        out["gain_bits"], out["gain"] = stored(g)
+    out["Wbar"] = out["Wbar_bits"] = None
+    if wbar == "shared":
+        out["Wbar_bits"], out["Wbar"] = stored(_normal_f32(_rng(seed, cfg.config_id, _WBAR), (V, d), cfg.w_sigma))
+    elif wbar == "per_head":
+        out["Wbar_bits"], out["Wbar"] = stored(
+            _normal_f32(_rng(seed, cfg.config_id, _WBAR), (max(K - 1, 0), V, d), cfg.w_sigma))
+    elif wbar != "none":
+        raise ValueError(f"unknown wbar {wbar!r}")
+    out["tau"] = (np.float32(0.5) + np.float32(1.5) * _rng(seed, cfg.config_id, _TAU).random(K, dtype=np.float32)
+                  ) if tau else None
+    out["bias"] = _normal_f32(_rng(seed, cfg.config_id, _BIAS), (K, V), 0.5) if bias else None
     return out

@@ -27,14 +27,16 @@ def call(**kw):
 def test_exports_match_header():
     names = B.header_functions()
     assert set(names) == {"solo_readout_abi_version", "solo_status_string", "solo_readout_workspace_size",
-                          "solo_readout_kernel_family", "solo_readout_fwd_bwd", "solo_readout_fwd_bwd_profiled"}
+                          "solo_readout_kernel_family", "solo_readout_fwd_bwd", "solo_readout_fwd_bwd_profiled",
+                          "solo_readout_general_workspace_size", "solo_readout_general",
+                          "solo_readout_exit_eval_workspace_size", "solo_readout_exit_eval"}
     lib = ctypes.CDLL(LIB)
     for n in names:
         assert hasattr(lib, n), n
     out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
     exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
     assert set(names) <= exported
-    assert B.abi_version() == 1
+    assert B.abi_version() == 2
 
 
 def test_status_strings():
@@ -44,22 +46,30 @@ def test_status_strings():
     assert B.status_string(99) == "unknown status"
 
 
-def test_workspace_has_no_TV_term():
-    # bf16 matrix-core family: Wg (V d 2) + rstd, lse, row_loss (3 K T 4) + final-module token
-    # records (T 16) + dgain partials (ceil(V/32) d 4)
-    def al(x):
-        return (x + 255) // 256 * 256
+def al(x):
+    return (x + 255) // 256 * 256
 
+
+def test_workspace_has_no_TV_term():
+    # bf16 matrix-core family: rstd, lse, row_loss (3 K T 4) + per-token records of
+    # every module (K T 16) + the terminal's gain-gradient partials (ceil(T/32) d 4)
+    # + the terminal's bf16 copy of gain * h (T d 2); no V x d and no T x V piece
     for K, T, d, V in [(4, 16384, 2048, 32000), (2, 32768, 2048, 128256), (4, 8192, 1024, 32000), (1, 1, 256, 1)]:
-        want = al(V * d * 2) + 3 * al(K * T * 4) + al(T * 16) + al(-(-V // 32) * d * 4)
+        want = 3 * al(K * T * 4) + al(K * T * 16) + al(-(-T // 32) * d * 4) + al(T * d * 2)
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, True) == want
-        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == al(V * d * 2) + 3 * al(K * T * 4)
-    # doubling T with V fixed grows the workspace by K*T*12 + T*16 bytes only
+        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == 3 * al(K * T * 4)
+    # the workspace does not depend on V at all
+    assert B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True) == \
+        B.workspace_size(4, 16384, 2048, 128256, B.SOLO_BF16, True)
+    # doubling T grows it by K T (12 + 16) + (T/32) d 4 + T d 2 bytes
     a = B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True)
     b = B.workspace_size(4, 32768, 2048, 32000, B.SOLO_BF16, True)
-    assert b - a == 3 * 4 * 16384 * 4 + 16384 * 16
-    # far below one module's T x V fp32 logits (2.1 GB at the 1B shape)
-    assert a < 16384 * 32000 * 4 / 4
+    assert b - a == 4 * 16384 * 28 + 512 * 2048 * 4 + 16384 * 2048 * 2
+    # well below one module's T x V fp32 logits (2.1 GB at the 1B shape)
+    assert a < 16384 * 32000 * 4 / 20
+    # vector-ALU family: 8-row token tiles, no per-token records
+    K, T, d, V = 2, 256, 64, 512
+    assert B.workspace_size(K, T, d, V, B.SOLO_F32, True) == 3 * al(K * T * 4) + al(-(-T // 8) * d * 4)
     # invalid arguments -> 0
     assert B.workspace_size(0, 8, 64, 32, B.SOLO_BF16, True) == 0
     assert B.workspace_size(1, 8, 63, 32, B.SOLO_BF16, True) == 0
@@ -132,3 +142,101 @@ def test_frozen_only_call_ignores_dW_pointers():
 def test_workspace_size_boundary():
     need = B.workspace_size(2, 8, 64, 32, B.SOLO_BF16, True)
     assert call(workspace_bytes=need - 1) == B.STATUS["SOLO_ERR_WORKSPACE"]
+
+
+# ---- solo_readout_general / solo_readout_exit_eval (host checks only)
+
+def gargs(**kw):
+    a = B.SoloReadoutArgs()
+    base = dict(K=3, T=40, d=256, V=100, dtype=B.SOLO_BF16, eps=1e-6, h=P, gain=P, W=P, targets=P, losses=P,
+                dh=P, dW=P, dgain=P, final_module_dW=1, workspace=P, workspace_bytes=WS)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(a, k, v)
+    return a
+
+
+def test_args_struct_layout_matches_header(tmp_path):
+    # offsets of every field as the C compiler lays the struct out
+    fields = [f for f, _ in B.SoloReadoutArgs._fields_]
+    src = tmp_path / "layout.c"
+    body = "\n".join(f'    printf("%s %zu\\n", "{f}", offsetof(solo_readout_args, {f}));' for f in fields)
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "solo_readout.h"\nint main(void) {\n'
+                   f'{body}\n    printf("size %zu\\n", sizeof(solo_readout_args));\n    return 0;\n}}\n')
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", f"-I{inc}", str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines())
+    for f in fields:
+        assert int(got[f]) == getattr(B.SoloReadoutArgs, f).offset, f
+    assert int(got["size"]) == ctypes.sizeof(B.SoloReadoutArgs)
+
+
+def test_general_workspace_sizes():
+    K, T, d, V = 3, 40, 256, 100
+    kt = K * T
+    tiles = -(-T // 32)
+    head = B.workspace_size(K, T, d, V, B.SOLO_BF16, True)
+    # the headline arguments through the general entry point: same workspace
+    assert B.general_workspace_size(gargs()) == head
+    # per-module gains: one partial slot per module
+    assert B.general_workspace_size(gargs(gain_per_module=1)) == \
+        3 * al(kt * 4) + al(kt * 16) + al(K * tiles * d * 4) + al(T * d * 2)
+    # temperature gradient: per-token shares
+    assert B.general_workspace_size(gargs(dtau=P)) == head + al(kt * 4)
+    # bias gradient without any readout gradient: records and gain * h copies of all K
+    # modules for the bias-gradient pass, no gain partials
+    assert B.general_workspace_size(gargs(final_module_dW=0, dW=0, dgain=0, dbias=P)) == \
+        3 * al(kt * 4) + al(kt * 16) + al(K * T * d * 2)
+    # PRIV: every module's copy
+    assert B.general_workspace_size(gargs(heads_train_readout=1, readout_per_head=1, Wbar=P, dWbar=P)) == \
+        head - al(T * d * 2) + al(K * T * d * 2)
+    # exit evaluation: per-token statistics only
+    assert B.exit_eval_workspace_size(gargs()) == 3 * al(kt * 4)
+    # rejected flags -> 0
+    assert B.general_workspace_size(gargs(gain_per_module=2)) == 0
+    assert B.general_workspace_size(gargs(K=0)) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=5), "SOLO_ERR_DTYPE"),
+    (dict(K=0), "SOLO_ERR_SHAPE"),
+    (dict(d=100), "SOLO_ERR_SHAPE"),
+    (dict(eps=-1.0), "SOLO_ERR_ARG"),
+    (dict(gain_per_module=3), "SOLO_ERR_ARG"),
+    (dict(readout_per_head=1), "SOLO_ERR_ARG"),                       # per-head readout without Wbar
+    (dict(heads_train_readout=1, Wbar=P), "SOLO_ERR_ARG"),            # PRIV without per-head readouts
+    (dict(h=0), "SOLO_ERR_NULL"),
+    (dict(dh=0), "SOLO_ERR_NULL"),
+    (dict(dW=0), "SOLO_ERR_NULL"),
+    (dict(dgain=0), "SOLO_ERR_NULL"),
+    (dict(final_module_dW=0, dgain=0, gain_per_module=1), "SOLO_ERR_NULL"),   # per-module gains need dgain
+    (dict(heads_train_readout=1, readout_per_head=1, Wbar=P, dWbar=0), "SOLO_ERR_NULL"),
+    (dict(Wbar=P + 8), "SOLO_ERR_ALIGN"),
+    (dict(tau=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(bias=P + 1), "SOLO_ERR_ALIGN"),
+    (dict(dtau=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(dbias=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(heads_train_readout=1, readout_per_head=1, Wbar=P, dWbar=P + 4), "SOLO_ERR_ALIGN"),
+    (dict(workspace_bytes=100), "SOLO_ERR_WORKSPACE"),
+])
+def test_general_validation_errors(kw, code):
+    assert B.readout_general_raw(gargs(**kw)) == B.STATUS[code]
+
+
+def test_general_null_args_pointer():
+    lib = B.load_library()
+    assert lib.solo_readout_general(None) == B.STATUS["SOLO_ERR_NULL"]
+    assert lib.solo_readout_exit_eval(None) == B.STATUS["SOLO_ERR_NULL"]
+    assert lib.solo_readout_general_workspace_size(None) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=0), "SOLO_ERR_NULL"),
+    (dict(losses=0), "SOLO_ERR_NULL"),
+    (dict(top1=P + 2), "SOLO_ERR_ALIGN"),
+    (dict(workspace_bytes=10), "SOLO_ERR_WORKSPACE"),
+])
+def test_exit_eval_validation_errors(kw, code):
+    # exit evaluation needs no gradient outputs: dh, dW, dgain may be NULL
+    assert B.exit_eval_raw(gargs(dh=0, dW=0, dgain=0, **kw)) == B.STATUS[code]
