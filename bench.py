@@ -30,6 +30,26 @@ PEAK_HBM_GBS = 8000.0
 METRIC = "readout fwd+bwd tokens/sec and % of bf16 MFMA peak (1B-class, V=32000)"
 
 
+# variant -> (input extras for solo_inputs.make_extras, call flags, description)
+VARIANTS = {
+    "headline": (None, dict(final_module_dW=True), "SOLO readout, one shared gain, tau = 1, no bias"),
+    "tau_bias": (dict(tau=True, bias=True),
+                 dict(final_module_dW=True, want_dtau=True, want_dbias=True),
+                 "SOLO readout with temperatures and biases and their gradients (heads' bias gradients "
+                 "through the bias-gradient pass)"),
+    "per_module_gain": (dict(per_module_gain=True, tau=True, bias=True),
+                        dict(final_module_dW=True, want_dtau=True, want_dbias=True),
+                        "per-module gains, temperatures and biases, all their gradients"),
+    "rand": (dict(wbar="per_head", tau=True, bias=True),
+             dict(final_module_dW=True, want_dtau=True, want_dbias=True),
+             "one frozen readout per head (RAND), temperatures and biases"),
+    "priv": (dict(wbar="per_head", tau=True, bias=True),
+             dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True),
+             "one trained readout per head (PRIV): every module's readout gradient"),
+    "exit_eval": (dict(), None, "forward-only exit evaluation: losses and top-1 of every exit"),
+}
+
+
 def _hip():
     import torch  # noqa: F401  (same HIP runtime as torch)
 
@@ -64,7 +84,7 @@ class EventSet:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
 
 
-def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
+def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "headline") -> dict:
     """fp64 oracle on the same workload restricted to sample_T tokens per module."""
     import numpy as np
 
@@ -83,8 +103,21 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
     h = x["h"].astype(np.float64)
     W = x["W"].astype(np.float64)
     g = x["gain"].astype(np.float64)
+    extras, flags, _ = VARIANTS[variant]
     t0 = time.perf_counter()
-    oracle.readout_fwd_bwd(h, g, W, x["targets"], True)
+    if extras is None:
+        oracle.readout_fwd_bwd(h, g, W, x["targets"], True)
+    else:
+        from solo_inputs import make_extras
+
+        e = make_extras(x, seed, **extras)
+        kw = dict(Wbar=e.get("Wbar"), tau=e.get("tau"), bias=e.get("bias"))
+        t0 = time.perf_counter()
+        if flags is None:
+            oracle.exit_eval(h, e["gain"], W, x["targets"], **kw)
+        else:
+            oracle.general_fwd_bwd(h, e["gain"], W, x["targets"], final_module_dW=flags.get("final_module_dW", True),
+                                   heads_train_readout=flags.get("heads_train_readout", False), **kw)
     dt = time.perf_counter() - t0
     cfg = x["cfg"]
     return {
@@ -93,7 +126,8 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0) -> dict:
         "cores": int(threads),
         "kind": "oracle",
         "sample": f"{cfg_name} shape with T={sample_T} tokens per module (K={cfg.K}, d={cfg.d}, V={cfg.V}, "
-                  f"final-module dW included), fp64 NumPy oracle, {dt:.2f} s",
+                  f"{'final-module dW included' if variant == 'headline' else 'variant ' + variant}), "
+                  f"fp64 NumPy oracle, {dt:.2f} s",
         "seconds": dt,
     }
 
@@ -130,6 +164,10 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="1b", help="workload shape (solo_inputs.CONFIGS key)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--variant", default="headline", choices=sorted(VARIANTS),
+                    help="headline: the shared-readout loss as the paper's headline runs it; the others time the "
+                         "general call (temperatures, biases, per-module gains, readout sources) or the "
+                         "forward-only exit evaluation on the same shapes")
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192,
                     help="tokens per module of the oracle's bounded sample (0 to skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_local_loss_1b.json"),
@@ -171,6 +209,27 @@ def main(argv=None) -> int:
         h, gain, W = (torch.from_numpy(x[k]).to(dev) for k in ("h", "gain", "W"))
         elem = 4
     targets = torch.from_numpy(x["targets"]).to(dev)
+    extras, flags, vdesc = VARIANTS[args.variant]
+    Wbar = tau = bias = None
+    if extras is not None:
+        from solo_inputs import make_extras
+
+        e = make_extras(x, args.seed, **extras)
+        bf = cfg.dtype == "bf16"
+
+        def up_any(name):
+            if e.get(name) is None:
+                return None
+            if bf:
+                return torch.from_numpy(np.ascontiguousarray(e[name + "_bits"]).view(np.int16)).view(
+                    torch.bfloat16).to(dev)
+            return torch.from_numpy(np.ascontiguousarray(e[name])).to(dev)
+
+        gain = up_any("gain")
+        Wbar = up_any("Wbar")
+        tau = torch.from_numpy(e["tau"]).to(dev) if e.get("tau") is not None else None
+        bias = torch.from_numpy(e["bias"]).to(dev) if e.get("bias") is not None else None
+        del e
     del x
     dt = binding.SOLO_BF16 if cfg.dtype == "bf16" else binding.SOLO_F32
     family = binding.kernel_family(K, T, d, V, dt)
@@ -181,19 +240,47 @@ def main(argv=None) -> int:
         dgain=torch.empty(d, dtype=torch.float32, device=dev),
         row_loss=None,
     )
-    ws = torch.empty(binding.workspace_size(K, T, d, V, dt, True), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     hip = _hip()
     n_ev = binding.NUM_STAGES + 1
     events = [EventSet(hip, n_ev) for _ in range(args.steps)]
+    gout = [None]
+    if args.variant == "headline":
+        ws = torch.empty(binding.workspace_size(K, T, d, V, dt, True), dtype=torch.uint8, device=dev)
+    else:
+        del out
+        # first call sizes and allocates the workspace and outputs; the timed calls reuse them
+        if flags is None:
+            r = binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, stream=stream)
+        else:
+            r = binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, stream=stream, **flags)
+        gout[0] = r
+        torch.cuda.synchronize()
+        a = binding._fill_inputs(h, gain, W, targets, Wbar, tau, bias, 1e-6)[0]
+        if flags is None:
+            nbytes = binding.exit_eval_workspace_size(a)
+        else:
+            a.final_module_dW = int(flags.get("final_module_dW", True))
+            a.heads_train_readout = int(flags.get("heads_train_readout", False))
+            a.dtau = 1 if flags.get("want_dtau") else None
+            a.dbias = 1 if flags.get("want_dbias") else None
+            nbytes = binding.general_workspace_size(a)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
 
     def step(ev=None):
         stage = None
         if ev is not None:
             assert hip.hipEventRecord(ctypes.c_void_p(ev.ev[0]), ctypes.c_void_p(stream.cuda_stream)) == 0
             stage = ev.ev[1:]
-        binding.readout_fwd_bwd(h, gain, W, targets, True, 1e-6, workspace=ws, out=out, stream=stream,
-                                stage_events=stage)
+        if args.variant == "headline":
+            binding.readout_fwd_bwd(h, gain, W, targets, True, 1e-6, workspace=ws, out=out, stream=stream,
+                                    stage_events=stage)
+        elif flags is None:
+            binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, workspace=ws, stream=stream,
+                              stage_events=stage, out=gout[0])
+        else:
+            binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, workspace=ws, stream=stream,
+                                    stage_events=stage, out=gout[0], **flags)
 
     for _ in range(args.warmup):
         step()
@@ -223,16 +310,23 @@ def main(argv=None) -> int:
     for e in events:
         e.destroy()
     ms_per_step = wall * 1e3 / args.steps
-    losses = out.losses.cpu().tolist()
+    losses = (out if args.variant == "headline" else gout[0]).losses.cpu().tolist()
     if not all(np.isfinite(losses)):
         print(f"non-finite losses {losses}", file=sys.stderr)
         return 1
 
-    alg_flops = costmodel.readout_flops(K, T, V, d, True)
+    is_eval = flags is None
+    fl = dict(final_module_dW=True) if is_eval else flags
+    alg_flops = costmodel.general_flops(K, T, V, d, final_module_dW=fl.get("final_module_dW", True),
+                                        heads_train_readout=fl.get("heads_train_readout", False), exit_eval=is_eval)
+    exe_flops = costmodel.executed_flops(K, T, V, d, final_module_dW=fl.get("final_module_dW", True),
+                                         heads_train_readout=fl.get("heads_train_readout", False),
+                                         bias_grad=fl.get("want_dbias", False), exit_eval=is_eval)
     tokens_per_s = T / (ms_per_step / 1e3)
-    # dominant kernel: the local-loss pass, 2r per token of every module (logits + input gradient)
+    # dominant kernel: the local-loss pass, 2r per token of every module (logits + input
+    # gradient), or the exit evaluation's forward pass (1r)
     ll_ms = stage_ms["local_loss"]
-    ll_flops = 2 * 2 * K * T * V * d
+    ll_flops = (1 if is_eval else 2) * 2 * K * T * V * d
     achieved = ll_flops / (ll_ms / 1e3) / 1e12
     traffic = None
     if os.path.exists(args.traffic):
@@ -240,7 +334,7 @@ def main(argv=None) -> int:
             with open(args.traffic) as f:
                 tr = json.load(f)
             # counters count only for the kernel source they were taken on
-            if (tr.get("config") == args.config and tr.get("family") == family
+            if (tr.get("config") == args.config and tr.get("family") == family and args.variant == "headline"
                     and tr.get("kernel_sources_sha256_16") == kernel_sources_hash()):
                 traffic = tr.get("bytes_per_launch")
         except Exception:
@@ -259,10 +353,13 @@ def main(argv=None) -> int:
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded N(0,1) hidden states, N(0,0.02^2) readout, 1+N(0,0.1^2) gain, Zipf(1.1) targets)",
-        "config": {"workload": f"{cfg.name}: K={K} modules, T={T} tokens/module, d={d}, V={V}, final-module dW",
-                   "K": K, "T": T, "d": d, "V": V, "kernel_family": family},
+        "config": {"workload": f"{cfg.name}: K={K} modules, T={T} tokens/module, d={d}, V={V}, "
+                               + ("final-module dW" if args.variant == "headline" else f"{args.variant}: {vdesc}"),
+                   "K": K, "T": T, "d": d, "V": V, "kernel_family": family, "variant": args.variant},
+        "executed_flops": exe_flops,
         "tflops_algorithmic": alg_flops / (ms_per_step / 1e3) / 1e12,
         "frac_bf16_peak_algorithmic": alg_flops / (ms_per_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+        "tflops_executed": exe_flops / (ms_per_step / 1e3) / 1e12,
         "module_tokens_per_s": K * tokens_per_s,
         "stage_ms": stage_ms,
         "event_ms_per_step": float(np.median(step_ms)),
@@ -273,7 +370,8 @@ def main(argv=None) -> int:
         "one_module_tv_bf16_bytes": int(T) * int(V) * 2,
         "roofline": {
             "bound": "mfma",
-            "kernel": "local-loss pass (logits + online log-sum-exp + dh), all K modules",
+            "kernel": ("exit evaluation (logits + online log-sum-exp + top-1), all K modules" if is_eval else
+                       "local-loss pass (logits + online log-sum-exp + dh), all K modules"),
             "achieved": achieved,
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
@@ -286,7 +384,7 @@ def main(argv=None) -> int:
         "losses": losses,
     }
     if args.cpu_sample_tokens > 0:
-        result["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample_tokens, args.seed)
+        result["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample_tokens, args.seed, args.variant)
     print(json.dumps(result), flush=True)
     return 0
 

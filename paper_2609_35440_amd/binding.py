@@ -311,11 +311,12 @@ def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps):
 def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, final_module_dW: bool = True,
                     heads_train_readout: bool = False, want_dtau: bool = False, want_dbias: bool = False,
                     eps: float = 1e-6, row_loss: bool = False, workspace=None, stream=None,
-                    stage_events=None) -> GeneralResult:
+                    stage_events=None, out: Optional[GeneralResult] = None) -> GeneralResult:
     """The loss with temperatures, biases, per-module gains and readout sources
     (``solo_readout_general``).  ``gain`` [d] or [K, d]; ``Wbar`` None, [V, d] or
     [K-1, V, d] (same dtype as h); ``tau`` [K] and ``bias`` [K, V] float32 or None.
-    Returns GeneralResult; gradients that were not requested are None.
+    Returns GeneralResult; gradients that were not requested are None.  ``out``
+    (a GeneralResult from an earlier call with the same arguments) reuses its tensors.
     """
     import torch
 
@@ -325,7 +326,7 @@ def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, fina
     f32 = dict(dtype=torch.float32, device=dev)
     fdw = bool(final_module_dW)
     priv = bool(heads_train_readout)
-    out = GeneralResult(
+    out = out if out is not None else GeneralResult(
         losses=torch.empty(K, **f32),
         dh=torch.empty_like(keep["h"]),
         dW=torch.empty((V, d), **f32) if fdw else None,
@@ -360,7 +361,8 @@ def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, fina
 
 
 def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float = 1e-6, row_loss: bool = True,
-              top1: bool = True, workspace=None, stream=None) -> EvalResult:
+              top1: bool = True, workspace=None, stream=None, stage_events=None,
+              out: Optional[EvalResult] = None) -> EvalResult:
     """Forward-only exit evaluation (``solo_readout_exit_eval``): losses [K],
     row_loss [K, T] and top1 [K, T] int32 (argmax of the logits, lowest index on ties)."""
     import torch
@@ -368,7 +370,7 @@ def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float
     a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
     K, T = a.K, a.T
     dev = h.device
-    out = EvalResult(
+    out = out if out is not None else EvalResult(
         losses=torch.empty(K, dtype=torch.float32, device=dev),
         row_loss=torch.empty((K, T), dtype=torch.float32, device=dev) if row_loss else None,
         top1=torch.empty((K, T), dtype=torch.int32, device=dev) if top1 else None,
@@ -386,6 +388,10 @@ def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     a.hip_stream = stream.cuda_stream or None
+    evs = None
+    if stage_events is not None:
+        evs = (ctypes.c_void_p * NUM_STAGES)(*[(e or None) for e in stage_events])
+        a.stage_events = ctypes.cast(evs, ctypes.c_void_p)
     st = exit_eval_raw(a)
     if st != 0:
         raise SoloError(st, status_string(st))

@@ -12,6 +12,8 @@ from __future__ import annotations
 
 __all__ = [
     "readout_flops",
+    "general_flops",
+    "executed_flops",
     "readout_bytes",
     "block_macs",
     "flops_per_token",
@@ -29,6 +31,39 @@ def readout_flops(K: int, T: int, V: int, d: int, final_module_dW: bool = True) 
     """
     units = 2 * K + (1 if final_module_dW else 0)
     return 2 * units * T * V * d
+
+
+def general_flops(K: int, T: int, V: int, d: int, *, final_module_dW: bool = True,
+                  heads_train_readout: bool = False, exit_eval: bool = False) -> int:
+    """Algorithmic FLOPs of the general call (the same units as readout_flops).
+
+    Every module costs 2r (logits + input gradient); a module whose readout is
+    trained (the terminal with final_module_dW, every head under PRIV) one r
+    more for the weight gradient.  Temperatures, biases and gains add only
+    O(T V) or O(T d) work.  Exit evaluation is the forward product alone: 1r
+    per module.
+    """
+    if exit_eval:
+        return 2 * K * T * V * d
+    trained = (1 if final_module_dW else 0) + ((K - 1) if heads_train_readout else 0)
+    return 2 * (2 * K + trained) * T * V * d
+
+
+def executed_flops(K: int, T: int, V: int, d: int, *, final_module_dW: bool = True,
+                   heads_train_readout: bool = False, bias_grad: bool = False, exit_eval: bool = False) -> int:
+    """Matrix-product FLOPs the fused kernels execute for the same call.
+
+    Local-loss pass: 2r per module (logits and the input-gradient product).
+    Readout-gradient pass: 2r per module in it (the logits again, with the
+    stored log-sum-exp, and the weight-gradient product).  Bias-gradient pass
+    (modules whose bias but not readout gets a gradient): 1r per module, the
+    logits again.  Exit evaluation: 1r per module.
+    """
+    if exit_eval:
+        return 2 * K * T * V * d
+    rg = (1 if final_module_dW else 0) + ((K - 1) if heads_train_readout else 0)
+    bg = (K - rg) if bias_grad else 0
+    return 2 * (2 * K + 2 * rg + bg) * T * V * d
 
 
 def readout_bytes(K: int, T: int, V: int, d: int, elem_bytes: int = 2, final_module_dW: bool = True) -> int:
