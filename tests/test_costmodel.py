@@ -68,3 +68,27 @@ def test_readout_flops_headline_value():
     assert cm.readout_flops(4, 16384, 32000, 2048) == 2 * 9 * 16384 * 32000 * 2048
     assert cm.readout_flops(4, 16384, 32000, 2048, final_module_dW=False) == 2 * 8 * 16384 * 32000 * 2048
     assert cm.readout_bytes(1, 1, 1, 8, 2) == 2 * 8 * 2 + 8 * 2 + 8 * 2 + 4 + 4 + 8 * 4 + 8 * 4
+
+
+def test_general_flops_special_cases():
+    from paper_2609_35440_amd import costmodel as cm
+
+    K, T, V, d = 4, 16384, 32000, 2048
+    r2 = 2 * T * V * d          # one readout unit (r MACs per token) in FLOPs
+    # the headline call is the paper's FLOP-table count: 2r per head, 3r for the terminal
+    assert cm.general_flops(K, T, V, d) == cm.readout_flops(K, T, V, d, True) == (2 * K + 1) * r2
+    assert cm.general_flops(K, T, V, d, final_module_dW=False) == cm.readout_flops(K, T, V, d, False)
+    # PRIV: every module pays 3r
+    assert cm.general_flops(K, T, V, d, heads_train_readout=True) == 3 * K * r2
+    # exit evaluation: the forward product of every exit
+    assert cm.general_flops(K, T, V, d, exit_eval=True) == K * r2
+    # executed: local pass 2r per module, readout-gradient pass 2r per trained readout,
+    # bias-gradient pass 1r for each other module
+    assert cm.executed_flops(K, T, V, d) == (2 * K + 2) * r2
+    assert cm.executed_flops(K, T, V, d, bias_grad=True) == (2 * K + 2 + (K - 1)) * r2
+    assert cm.executed_flops(K, T, V, d, heads_train_readout=True, bias_grad=True) == 4 * K * r2
+    assert cm.executed_flops(K, T, V, d, final_module_dW=False, bias_grad=True) == 3 * K * r2
+    assert cm.executed_flops(K, T, V, d, exit_eval=True) == K * r2
+    # 1B headline: 19.33 TFLOP algorithmic, 21.47 executed
+    assert abs(cm.general_flops(K, T, V, d) / 1e12 - 19.33) < 0.01
+    assert abs(cm.executed_flops(K, T, V, d) / 1e12 - 21.47) < 0.01
