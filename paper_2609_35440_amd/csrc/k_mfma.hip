@@ -69,17 +69,17 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
 
 // MODE LOCAL / EVAL: grid (ceil(T/32), K); module k = blockIdx.y.
 // MODE RGRAD / BGRAD: grid (ceil(V/32), nmod); module k = m0 + blockIdx.y.
-// EXT (LOCAL only): the variant with per-chunk biases and the running sums
-// of the temperature gradient; EVAL always handles biases.
+// EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     using G = Geo<DS>;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
     constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
-    constexpr bool DT = MODE == LOCAL && EXT;               // temperature-gradient sums
-    // the stream of a chunk is issued in batches [0, kDma1), [kDma1, kDma2), [kDma2, NI)
-    constexpr int kDma1 = (3 * G::NI + 7) / 8, kDma2 = (6 * G::NI + 7) / 8;
+    // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
+    // the logit products, [kDmaA, NI) after the elementwise step (at d = 2048:
+    // 5 and 3 of 8; measured best of 3..8 inside the products)
+    constexpr int kDmaA = (5 * G::NI + 7) / 8;
     // Separate LDS objects, so that the compiler can tell the chunk being read
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
@@ -186,7 +186,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
     // online softmax state (LL, base 2), per lane: row xo, streamed column yy
     float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
-    float su_part = 0.f, sy_part = 0.f;   // DT: sum_v e^(z - m) sxy_v, and sxy of the target (u = r sxy)
     float best = -INFINITY;               // EVAL: largest logit seen by this lane, and its column
     int best_v = -1;
     float db_part = 0.f;                  // RGRAD / BGRAD: sum_t (p - onehot) for row xo
@@ -204,27 +203,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---- split-K partial of the logit tile S[y][x] over this wave's columns.
         // All operand reads go out first, ahead of the data of the next chunk,
-        // whose stream is issued in three batches (here, after these products
-        // and after the elementwise step) so that neither the texture unit's
-        // queue nor the LDS write port sees the whole chunk at once.
-        // (the extended variant at the widest slices holds 6 of them at a time:
+        // whose stream is spread over the products and the end of the
+        // elementwise step, so that neither the texture unit's queue nor the
+        // LDS write port sees the whole chunk at once.
+        // (the bias variant at the widest slices holds 5 of them at a time:
         // each later read refills the registers of the products just issued)
-        constexpr int RA = (DT && G::NK > 6) ? 6 : G::NK;
+        constexpr int RA = (BZ && MODE == LOCAL && G::NK > 5) ? 5 : G::NK;
         bf16x8 ay[RA];
 #pragma unroll
         for (int kk = 0; kk < RA; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
-        if (more) {
-            stream.template issue_range<0, kDma1>(nrs, d, nxt);
-            issue_side(y0 + YC, side_nxt);
-        }
+        if (more) issue_side(y0 + YC, side_nxt);
         f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
             S0 = mfma16(ay[kk % RA], xr[0][kk], S0);
             S1 = mfma16(ay[kk % RA], xr[1][kk], S1);
             if (kk + RA < G::NK) ay[kk % RA] = *(LDS_AS bf16x8*)(cur + a_off + 64 * (kk + RA));
+            if (kk < kDmaA) {
+                if (more) stream.issue_one(nrs, d, nxt, kk);
+                __builtin_amdgcn_sched_barrier(0);  // keeps the instruction between these products
+            }
         }
-        if (more) stream.template issue_range<kDma1, kDma2>(nrs, d, nxt);
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
         *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
         *(f32x4*)(part + (w * XR + 16 + (lane & 15)) * PP + 4 * (lane >> 4)) = S1;
@@ -250,17 +249,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 if (cmax > m_run + kLazyThresh2) {
                     alpha = __builtin_amdgcn_exp2f(m_run - cmax);
                     s_part *= alpha;
-                    if (DT) su_part *= alpha;
                     m_run = cmax;
                 }
             }
             const float p = __builtin_amdgcn_exp2f(zc - m_run);
             s_part += p;
-            if (DT) su_part = __builtin_fmaf(p, sxy, su_part);
-            if (yg == own_tgt) {
-                zy_part = zc;
-                if (DT) sy_part = sxy;
-            }
+            if (yg == own_tgt) zy_part = zc;
             if (MODE == EVAL && zc > best) {  // strict: the first (lowest) column keeps a tie
                 best = zc;
                 best_v = yg;
@@ -278,7 +272,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             db_part += dlt;
         }
         if (PC) gbuf[xo * YC + yy] = (bf16)gval;
-        if (more) stream.template issue_range<kDma2, G::NI>(nrs, d, nxt);
+        if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
         lds_barrier();
 
         if (PC) {
@@ -325,8 +319,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // finish the online softmax of rows 4w..4w+3
         const float s = row16_sum(s_part);
         const float zy = row16_sum(zy_part);
-        const float su = DT ? row16_sum(su_part) : 0.f;
-        const float sy = DT ? row16_sum(sy_part) : 0.f;
         if (MODE == EVAL) {
             // argmax over the 16 lanes of the row: larger logit, then lower column
 #pragma unroll
@@ -353,8 +345,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), r_row * tau_k * a.inv_T};
                     *(f32x4*)(a.rowrec + 4 * t) = rec4;
                 }
-                // d loss / d tau per token: (sum_v p_v u_v - u_y) / T with u = r sxy
-                if (DT && a.rowdtau) a.rowdtau[t] = tok ? r_row * (su / s - sy) * a.inv_T : 0.f;
             }
             sbuf[xo] = 1.f / s;
         }
@@ -367,13 +357,16 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         const int tgt = xok ? a.targets[modoff + xg] : -1;
         const bool tok = tgt >= 0 && tgt < nY;
         const float inv_s = sbuf[ex];
-        const float scale = tau_k * a.inv_T;
+
         const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
         const bf16* wrow = Rk + (long long)(tok ? tgt : 0) * d;
         const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
         float* dgp = want_dg ? a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d
                              : nullptr;
-        // sweep 1: acc <- dhhat = tau (acc / s - R_y) / T and the row sums of dn * n (dn = g dhhat, n = r h)
+        // sweep 1: acc <- e = (acc / s - R_y) / T, so that dhhat = tau e, and the
+        // row sums of e * g * n (n = r h).  That row sum is both the RMSNorm
+        // backward's mean(dn * n) = tau sum / d and the token's share of
+        // d loss / d tau = sum_v delta_v u_v = <sum_v delta_v R_v, g * n>.
         float cp = 0.f;
 #pragma unroll
         for (int b = 0; b < (PC ? G::NB : 1); ++b) {
@@ -388,9 +381,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const float wy = tok ? bf16_bits_to_f32(wv[e]) : 0.f;
-                    const float dhat = (acc[b][4 * i4 + e] * inv_s - wy) * scale;
-                    cp += bf16_bits_to_f32(gv[e]) * dhat * (rx * bf16_bits_to_f32(hv[e]));
-                    acc[b][4 * i4 + e] = dhat;
+                    const float ev = (acc[b][4 * i4 + e] * inv_s - wy) * a.inv_T;
+                    cp += bf16_bits_to_f32(gv[e]) * ev * (rx * bf16_bits_to_f32(hv[e]));
+                    acc[b][4 * i4 + e] = ev;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);  // one block's loads at a time
@@ -401,7 +394,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         float csum = 0.f;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + ex];
-        const float cmean = csum / (float)d;
+        const float cmean = tau_k * csum / (float)d;
+        if (a.rowdtau && w == 0 && ehh == 0 && xok) a.rowdtau[modoff + xg] = tok ? csum : 0.f;
 
         // sweep 2: dh = r (dn - c n)
         if (xok) {
@@ -417,7 +411,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float n = rx * bf16_bits_to_f32(hv[e]);
-                        o[e] = (bf16)(rx * (bf16_bits_to_f32(gv[e]) * acc[b][4 * i4 + e] - cmean * n));
+                        o[e] = (bf16)(rx * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][4 * i4 + e] - cmean * n));
                     }
                     *(bf16x4*)(dhrow + j) = o;
                 }
@@ -425,7 +419,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
         }
         // sweep 3, for a module that trains its gain: the tile's partial sums
-        // of dhhat * n over its 32 rows (the 16-lane row, then the other row
+        // of dhhat * n = tau e * n over its 32 rows (the 16-lane row, then the other row
         // of the half-wave)
         if (want_dg) {
 #pragma unroll
@@ -437,7 +431,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     f32x4 pv;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float t = row16_sum(acc[b][4 * i4 + e] * (rx * bf16_bits_to_f32(hv[e])));
+                        const float t = row16_sum(tau_k * acc[b][4 * i4 + e] * (rx * bf16_bits_to_f32(hv[e])));
                         pv[e] = t + __shfl_xor(t, 16, 64);
                     }
                     if (ex == 0) *(f32x4*)(dgp + j) = pv;

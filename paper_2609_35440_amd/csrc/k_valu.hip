@@ -79,7 +79,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
     // elementwise step: thread (sr = tid/32, sq = tid%32) handles columns sq and sq + 32 of row sr
     const int sr = tid >> 5;
     const int sq = tid & 31;
-    float m_run = -INFINITY, s_run = 0.f, zy = 0.f, su = 0.f, uy = 0.f;
+    float m_run = -INFINITY, s_run = 0.f, zy = 0.f;
     float best = -INFINITY;
     int best_v = -1;
     float dbp = 0.f;
@@ -134,10 +134,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                     best = z[hh];
                     best_v = yg;
                 }
-                if (yg == own_tgt) {
-                    zy = z[hh];
-                    uy = u[hh];
-                }
+                if (yg == own_tgt) zy = z[hh];
             }
             float cmax = fmaxf(z[0], z[1]);
             for (int off = 16; off > 0; off >>= 1) cmax = fmaxf(cmax, __shfl_xor(cmax, off, 32));
@@ -146,13 +143,9 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             m_run = m_new;
             const float p0 = (z[0] == -INFINITY) ? 0.f : __expf(z[0] - m_run);
             const float p1 = (z[1] == -INFINITY) ? 0.f : __expf(z[1] - m_run);
-            float ps = p0 + p1, pu = p0 * u[0] + p1 * u[1];
-            for (int off = 16; off > 0; off >>= 1) {
-                ps += __shfl_xor(ps, off, 32);
-                pu += __shfl_xor(pu, off, 32);
-            }
+            float ps = p0 + p1;
+            for (int off = 16; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 32);
             s_run = s_run * alpha + ps;
-            su = su * alpha + pu;
             sS[sr * YC + sq] = p0;
             sS[sr * YC + sq + 32] = p1;
             if (sq == 0) sc[sr] = alpha;
@@ -204,10 +197,9 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
     }
 
     if (LL) {
-        // finish rows: lse, row loss, d loss / d tau, top-1; the target logit sits in one thread of the row group
+        // finish rows: lse, row loss, top-1; the target logit sits in one thread of the row group
         for (int off = 16; off > 0; off >>= 1) {
             zy += __shfl_xor(zy, off, 32);
-            uy += __shfl_xor(uy, off, 32);
             if (MODE == EVAL) {
                 const float ob = __shfl_xor(best, off, 32);
                 const int ov = __shfl_xor(best_v, off, 32);
@@ -225,14 +217,15 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                 a.lse[t] = lse;
                 a.rowloss[t] = tok ? lse - zy : __int_as_float(0x7fc00000);
                 if (MODE == EVAL && a.top1) a.top1[t] = best_v;
-                if (MODE == LOCAL && a.rowdtau) a.rowdtau[t] = tok ? (su / s_run - uy) * a.inv_T : 0.f;
             }
             sc[sr] = 1.f / s_run;
         }
         __syncthreads();
     }
     if (MODE == LOCAL) {
-        // dhat = tau (acc / s - R_y) / T; dn = g dhat; c = mean(dn n); dh = r (dn - c n)
+        // e = (acc / s - R_y) / T, dhat = tau e, dn = g dhat; the row sum of
+        // e g n is both tau^-1 d mean(dn n) and the token's d loss / d tau
+        // (sum_v delta_v u_v = <sum_v delta_v R_v, g n>); dh = r (dn - c n)
         const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
         float dgp[NQ];
 #pragma unroll
@@ -250,12 +243,12 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                 const int j = tid + NTHR * q;
                 if (j < d) {
                     const float wy = tok ? ld(Rk, (long long)tg * d + j) : 0.f;
-                    const float dhat = (acc[r][q] * sc[r] - wy) * tau * a.inv_T;
+                    const float ev = (acc[r][q] * sc[r] - wy) * a.inv_T;
                     const float n = (xg < nX) ? rx * ld(hk, (long long)xg * d + j) : 0.f;
-                    const float dn = ld(gk, j) * dhat;
-                    acc[r][q] = dn;
-                    cp[r] = fmaf(dn, n, cp[r]);
-                    dgp[q] = fmaf(dhat, n, dgp[q]);
+                    const float gj = ld(gk, j);
+                    acc[r][q] = tau * gj * ev;          // dn
+                    cp[r] = fmaf(gj * ev, n, cp[r]);
+                    dgp[q] = fmaf(tau * ev, n, dgp[q]);
                 }
             }
             float v = cp[r];
@@ -277,7 +270,11 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             if (xg >= nX) continue;
             float csum = 0.f;
             for (int i = 0; i < NTHR / 64; ++i) csum += red[r * (NTHR / 64) + i];
-            const float cmean = csum / (float)d;
+            const float cmean = tau * csum / (float)d;
+            if (a.rowdtau && tid == 0) {
+                const int tg = a.targets[modoff + xg];
+                a.rowdtau[modoff + xg] = (tg >= 0 && tg < nY) ? csum : 0.f;
+            }
             const float rx = a.rstd[modoff + xg];
             E* out = (E*)a.dh + (modoff + xg) * (long long)d;
 #pragma unroll

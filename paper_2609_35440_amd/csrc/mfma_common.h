@@ -138,6 +138,12 @@ struct ChunkStream {
         }
     }
 
+    // instruction q alone (q a constant after unrolling)
+    __device__ __forceinline__ void issue_one(i32x4 rs, int d, unsigned slice, int q) const {
+        const int voffset = voff[layout::stream_vidx<DS>(q)] + layout::stream_row0<DS>(q) * d * 2;
+        buffer_load_lds16(rs, slice + layout::stream_lds_off<DS>(q), voffset);
+    }
+
     // stream rows y0 .. y0 + 15 (this wave's DS columns) of Y into `slice`
     __device__ __forceinline__ void issue(const bf16* __restrict__ Y, int nY, int d, int y0, unsigned slice) const {
         issue_range<0, G::NI>(rsrc(Y, nY, d, y0), d, slice);

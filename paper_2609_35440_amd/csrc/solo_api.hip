@@ -26,7 +26,7 @@ bool flag_ok(int f) { return f == 0 || f == 1; }
 struct Plan {
     bool mfma = false;
     bool eval = false;
-    bool ext = false;          // local-loss variant with biases and temperature-gradient sums
+    bool ext = false;          // local-loss variant with per-chunk biases
     int dg_mode = 0;           // 0 none, 1 terminal only, 2 every module
     int slots = 0;             // gain-gradient partial slots
     int ntiles = 0;            // token tiles of the local-loss pass
@@ -79,7 +79,7 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
             P->bg_hi = K - 1;
         }
     }
-    P->ext = a.bias != nullptr || a.dtau != nullptr;
+    P->ext = a.bias != nullptr;
     P->dg_mode = a.gain_per_module ? 2 : (fdw ? 1 : 0);
     P->slots = P->dg_mode == 2 ? K : (P->dg_mode == 1 ? 1 : 0);
     const int rows = P->mfma ? solo::kMfmaRows : solo::kValuRows;

@@ -63,8 +63,8 @@ hipError_t launch_module_sum(const float* rows, float* out, int K, int T, double
 // dgain[slot][j] = sum over tiles of part[slot][tile][j], fixed order
 hipError_t launch_dgain_reduce(const float* part, float* dgain, int slots, int ntiles, int d, hipStream_t s);
 
-// fused passes; `ext` selects the local-loss variant with bias and temperature
-// gradient, `nmod` is the number of modules of a readout-/bias-gradient launch
+// fused passes; `ext` selects the local-loss variant with per-chunk biases,
+// `nmod` is the number of modules of a readout-/bias-gradient launch
 bool mfma_supported(int dtype, int d);
 hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s);
 hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s);
