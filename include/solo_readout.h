@@ -89,10 +89,10 @@ size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int fi
 
 /*
  * Name of the kernel family one call with these sizes runs on:
- * "mfma" (bf16 matrix-core kernels) or "valu" (fp32 vector-ALU kernels,
- * used for SOLO_F32 and for bf16 widths the matrix-core kernels do not tile:
- * d not a multiple of 256, or d > 2048).  Returns "invalid" for arguments
- * solo_readout_fwd_bwd would reject.
+ * "mfma" (bf16 matrix-core kernels, 32-row tiles: d a multiple of 256 up to
+ * 2048), "mfma_wide" (bf16 matrix-core kernels, 16-row tiles: d = 2560) or
+ * "valu" (fp32 vector-ALU kernels, used for SOLO_F32 and for every other bf16
+ * width).  Returns "invalid" for arguments solo_readout_fwd_bwd would reject.
  */
 const char* solo_readout_kernel_family(int K, int T, int d, int V, int dtype);
 

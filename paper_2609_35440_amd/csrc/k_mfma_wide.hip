@@ -1,0 +1,457 @@
+// Fused matrix-core passes of the SOLO shared-readout loss for wide hidden
+// states, d = 2560 (bf16 operands, fp32 accumulate, gfx950).
+//
+// Same passes and algebra as k_mfma.hip: module k predicts through its
+// readout R_k, gain g_k, temperature tau_k and bias b_k (Eq. 2 of the paper,
+// with the bias of Algorithm 1):  z_tv = tau_k r_t <R_kv, g_k * h_t> + b_kv.
+// What the width changes is what fits on a CU:
+//
+//   - 16 stationary rows per workgroup instead of 32: wave w owns the d/8
+//     columns [w d/8, (w+1) d/8) of a 16 x d/8 fp32 accumulator (80 registers
+//     per lane at d = 2560) and of the stationary operand;
+//   - the second product runs on the 16x16x16 instruction (its contraction
+//     over the 16 streamed rows of a chunk), its streamed operand read with
+//     one ds_read_b64_tr_b16 per product;
+//   - one chunk is 16 x d bf16 = 80 KiB at d = 2560, so two of them do not
+//     fit next to the partial-logit exchange in 160 KiB of LDS.  The chunk
+//     lives in one LDS buffer, and the next one is staged through registers:
+//     row-contiguous global loads are issued a whole chunk ahead, and written
+//     to LDS once the current chunk's last read has returned.
+//
+// Per chunk each wave (1) reads its slice row-wise and computes its split-K
+// partial of the 16x16 logit tile; (2) the 8 partials meet in LDS and each
+// wave finishes the elementwise step for 2 of the 16 stationary rows;
+// (3) every wave accumulates its column slice of the second product; then
+// (4) it writes the staged next chunk into its slice and stages the one after.
+#include "mfma_common.h"
+#include "mfma_layout_wide.h"
+
+namespace solo {
+
+namespace {
+
+using namespace mfma;
+
+constexpr int NW = layoutw::NW;  // waves per workgroup
+constexpr int NTHR = NW * 64;
+constexpr int XR = kMfmaWideRows;  // stationary rows per workgroup (16)
+constexpr int YC = layoutw::YC;    // streamed rows per chunk
+constexpr int PP = 20;             // row pitch (floats) of the partial logit tiles
+
+static_assert(XR == 16, "one 16-row block of stationary rows");
+
+enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
+
+template <int DS>
+struct Geo : layoutw::Geo<DS> {
+    static constexpr int NK = DS / 32;  // 32-deep k-steps of the logit product
+    static constexpr int NB = DS / 16;  // 16-column accumulator blocks per wave
+    static constexpr int YBUF = NW * layoutw::Geo<DS>::SLICE;
+    static constexpr int TOTAL = YBUF + NW * XR * PP * 4 + XR * YC * 2 + 2 * XR * 4 + NW * XR * 4 + 2 * YC * 16;
+    static_assert(TOTAL <= 160 * 1024, "LDS budget");
+};
+
+typedef __bf16 bf16x4w __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16k16(bf16x4w a, bf16x4w b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
+    return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
+}
+
+// MODE LOCAL / EVAL: grid (ceil(T/16), K); module k = blockIdx.y.
+// MODE RGRAD / BGRAD: grid (ceil(V/16), nmod); module k = m0 + blockIdx.y.
+// EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
+template <int MODE, int DS, bool EXT>
+__global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
+    using G = Geo<DS>;
+    constexpr bool LL = MODE == LOCAL || MODE == EVAL;           // X = h, Y = readout
+    constexpr bool PC = MODE == LOCAL || MODE == RGRAD;          // second product
+    constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
+    constexpr int RA = 4;                                        // row-wise reads in flight
+    __shared__ __attribute__((aligned(16))) char ybuf[G::YBUF];
+    __shared__ __attribute__((aligned(16))) float part[NW * XR * PP];
+    __shared__ __attribute__((aligned(16))) bf16 gbuf[XR * YC];
+    __shared__ float abuf[XR];
+    __shared__ float sbuf[XR];
+    __shared__ float cbuf[NW * XR];
+    __shared__ __attribute__((aligned(16))) float recA[YC * 4];
+    __shared__ __attribute__((aligned(16))) float recB[YC * 4];
+
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int d = a.d;
+    const int js = w * DS;
+    const int x0 = blockIdx.x * XR;
+    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
+    const long long modoff = (long long)k * a.T;
+    const float tau_k = a.tau ? a.tau[k] : 1.f;
+
+    const bf16* __restrict__ hk = (const bf16*)a.h + modoff * d;
+    const bf16* __restrict__ Rk = readout_of(a, k);
+    const bf16* __restrict__ gk = (const bf16*)a.gain + (long long)k * a.g_stride;
+    const bf16* __restrict__ X = LL ? hk : Rk;
+    const bf16* __restrict__ Y = LL ? Rk : (const bf16*)a.hg + (long long)(k - a.hg_m0) * a.T * d;
+    const int nX = LL ? a.T : a.V;
+    const int nY = LL ? a.V : a.T;
+    const int nchunks = (nY + YC - 1) / YC;
+
+    LDS_AS char* slice = (LDS_AS char*)(LDS_AS void*)ybuf + w * G::SLICE;
+
+    // elementwise ownership: lanes l and l + 32 both compute stationary row
+    // xo, streamed column yy; only l < 32 writes
+    const int xo = 2 * w + ((lane >> 4) & 1);
+    const int yy = lane & 15;
+    const bool wr = lane < 32;
+    float own_r2 = 0.f;  // LL: r_t tau_k log2 e of row xo
+    int own_tgt = -1;    // LL: target of row xo
+    if (LL && x0 + xo < nX) {
+        own_r2 = a.rstd[modoff + x0 + xo] * tau_k * kLog2e;
+        own_tgt = a.targets[modoff + x0 + xo];
+    }
+    float bx2 = 0.f;  // RGRAD / BGRAD: bias of the stationary readout row, base 2
+    if (!LL && a.bias && x0 + xo < nX) bx2 = a.bias[(long long)k * a.V + x0 + xo] * kLog2e;
+    const bool has_bias = a.bias != nullptr;
+
+    // ---- staged stream: lane p of load q fetches slot 64 q + p of the wave's
+    // slice (row-contiguous), with zeros past the last streamed row
+    i32x4 stg[G::NI];
+    auto stage_load = [&](int y0) __attribute__((always_inline)) {
+        const int rows = nY - y0 < YC ? nY - y0 : YC;
+        const int rem = rows > 0 ? rows * d * 2 - 2 * js : 0;  // rows of this chunk only
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(Y + (long long)(rows > 0 ? y0 : 0) * d + js), (short)0, rem > 0 ? rem : 0, 0x00020000);
+#pragma unroll
+        for (int q = 0; q < G::NI; ++q) {
+            const int off = (layoutw::stage_row<DS>(q, lane) * d + 8 * layoutw::stage_gran<DS>(q, lane)) * 2;
+            stg[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+        }
+    };
+    auto stage_store = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < G::NI; ++q) *(LDS_AS i32x4*)(slice + layoutw::stage_dst<DS>(q, lane)) = stg[q];
+    };
+
+    const unsigned recA_u = lds_addr((LDS_AS char*)(LDS_AS void*)recA);
+    const unsigned recB_u = lds_addr((LDS_AS char*)(LDS_AS void*)recB);
+    auto issue_side = [&](int y0, unsigned dst) __attribute__((always_inline)) {
+        const int rows = nY - y0;
+        if (!LL && w == 0 && lane < YC) {
+            // the 16 per-token records of the chunk
+            const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
+            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, lane * 16);
+        }
+        if (BZ && has_bias && w == 0 && lane < YC) {
+            // the 16 biases of the chunk (zeros past the vocabulary)
+            const unsigned rem = rows > 0 ? (unsigned)rows * 4u : 0u;
+            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, lane * 4);
+        }
+    };
+
+    // first chunk: side data, staged load, then its LDS write; the second chunk staged
+    issue_side(0, recA_u);
+    stage_load(0);
+    wait_vm();
+    stage_store();
+    if (nchunks > 1) stage_load(YC);
+
+    // stationary operand (local loss and exit evaluation: times the gain,
+    // rounded once): B of the 16x16x32 logit product, lane holds
+    // X[x0 + lane%16][js + 32 kk + 8 (lane/16) .. +7]
+    bf16x8 xr[G::NK];
+#pragma unroll
+    for (int kk = 0; kk < G::NK; ++kk) {
+        const int j0 = js + 32 * kk + 8 * (lane >> 4);
+        const bf16x8 gv = *(const bf16x8*)(gk + j0);
+        const int xrow = x0 + (lane & 15);
+        bf16x8 xv;
+        if (xrow < nX) {
+            xv = *(const bf16x8*)(X + (long long)xrow * d + j0);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) xv[e] = (bf16)0.f;
+        }
+        if (LL) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) xr[kk][e] = (bf16)((float)xv[e] * (float)gv[e]);
+        } else {
+            xr[kk] = xv;
+        }
+    }
+
+    f32x4 acc[PC ? G::NB : 1];
+#pragma unroll
+    for (int b = 0; b < (PC ? G::NB : 1); ++b) acc[b] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+    // online softmax state (LL, base 2), per lane: row xo, streamed column yy
+    float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
+    float best = -INFINITY;  // EVAL: largest logit seen by this lane, and its column
+    int best_v = -1;
+    float db_part = 0.f;     // RGRAD / BGRAD: sum_t (p - onehot) for row xo
+
+    // row-wise read of k-step kk at rd_even + 64 kk (kk even) or rd_odd + 64 kk (kk odd):
+    // the swizzle flips bit 2 of the granule index for rows with (r & 4)
+    const int rd_even = layoutw::rowread_off<DS>(lane, 0);
+    const int rd_odd = layoutw::rowread_off<DS>(lane, 1) - 64;
+
+    auto step = [&](LDS_AS float* side, unsigned side_nxt, int c) __attribute__((always_inline)) {
+        const int y0 = c * YC;
+        const bool more = c + 1 < nchunks;
+
+        // ---- (1) split-K partial of the logit tile S[y][x] over this wave's columns
+        bf16x8 ay[RA];
+#pragma unroll
+        for (int kk = 0; kk < RA && kk < G::NK; ++kk)
+            ay[kk] = *(LDS_AS bf16x8*)(slice + ((kk & 1) ? rd_odd : rd_even) + 64 * kk);
+        if (more) issue_side(y0 + YC, side_nxt);
+        f32x4 S0 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < G::NK; ++kk) {
+            const bf16x8 wa = ay[kk % RA];
+            if (kk + RA < G::NK)
+                ay[kk % RA] = *(LDS_AS bf16x8*)(slice + (((kk + RA) & 1) ? rd_odd : rd_even) + 64 * (kk + RA));
+            S0 = mfma16(wa, xr[kk], S0);
+        }
+        // C layout: lane holds S[y = 4 (lane/16) + i][x = lane%16]; store as part[w][x][y]
+        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
+        lds_barrier();
+
+        // ---- (2) elementwise step for rows xo = 2w, 2w+1 (lane: row xo, column yy)
+        float q[NW];
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + yy];
+        static_assert(NW == 8, "partial-sum tree");
+        const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
+        const int yg = y0 + yy;
+        float gval = 0.f;
+        if (LL) {
+            // columns past the end of the vocabulary get z = -inf
+            float ymask = (yg < nY) ? 0.f : -INFINITY;
+            if (BZ && has_bias) ymask += side[yy] * kLog2e;
+            const float zc = __builtin_fmaf(sxy, own_r2, ymask);
+            float alpha = 1.f;
+            if (__builtin_expect(__any(zc > m_run + kLazyThresh2), 0)) {  // wave-uniform
+                const float cmax = row16_max(zc);
+                if (cmax > m_run + kLazyThresh2) {
+                    alpha = __builtin_amdgcn_exp2f(m_run - cmax);
+                    s_part *= alpha;
+                    m_run = cmax;
+                }
+            }
+            const float p = __builtin_amdgcn_exp2f(zc - m_run);
+            s_part += p;
+            if (yg == own_tgt) zy_part = zc;
+            if (MODE == EVAL && zc > best) {  // strict: the first (lowest) column keeps a tie
+                best = zc;
+                best_v = yg;
+            }
+            gval = p;
+            if (MODE == LOCAL && wr) abuf[xo] = alpha;  // the 16 lanes of a row store the same value
+        } else {
+            // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
+            // the end of the module read as zeros and are masked
+            const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2 - r4[0]));
+            // (a padded token's zero record would match readout row 0 as its target)
+            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f) : 0.f;
+            gval = dlt * r4[3];
+            db_part += dlt;
+        }
+        if (PC && wr) gbuf[xo * YC + yy] = (bf16)gval;
+        lds_barrier();
+
+        if (PC) {
+            // ---- (3) second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
+            // B operand: lane holds G[x = lane%16][y = 4 (lane/16) .. +3]
+            const bf16x4w gfrag = *(LDS_AS bf16x4w*)(gbuf + (lane & 15) * YC + 4 * (lane >> 4));
+            if (MODE == LOCAL) {
+                const float al = abuf[lane & 15];
+                if (__any(al != 1.f)) {
+#pragma unroll
+                    for (int b = 0; b < G::NB; ++b) acc[b] *= al;
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b) {
+                const bf16x4w t = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                    (LDS_AS bf16x4w*)(slice + layoutw::trread_off<DS>(lane, b)));
+                acc[PC ? b : 0] = mfma16k16(t, gfrag, acc[PC ? b : 0]);
+            }
+        }
+        // ---- (4) the next chunk into the slice once this chunk's reads have returned
+        // (LDS operations of a wave run in order); its side data and staged
+        // loads have landed after the vmcnt wait; then stage the chunk after it
+        wait_vm();
+        if (more) {
+            stage_store();
+            __builtin_amdgcn_sched_barrier(0);
+            if (c + 2 < nchunks) stage_load(y0 + 2 * YC);
+        }
+    };
+
+    for (int c = 0; c < nchunks; c += 2) {
+        step((LDS_AS float*)(LDS_AS void*)recA, recB_u, c);
+        if (c + 1 < nchunks) step((LDS_AS float*)(LDS_AS void*)recB, recA_u, c + 1);
+    }
+
+    // ---- epilogues.  acc[b] lane layout: x = lane%16, j = js + 16 b + 4 (lane/16) + i
+    const int ex = lane & 15;
+    const int eg = lane >> 4;
+    if (LL) {
+        // finish the online softmax of rows 2w, 2w+1
+        const float s = row16_sum(s_part);
+        const float zy = row16_sum(zy_part);
+        if (MODE == EVAL) {
+            // argmax over the 16 lanes of the row: larger logit, then lower column
+#pragma unroll
+            for (int off = 1; off < 16; off <<= 1) {
+                const float ob = __shfl_xor(best, off, 64);
+                const int ov = __shfl_xor(best_v, off, 64);
+                if (ob > best || (ob == best && (unsigned)ov < (unsigned)best_v)) {
+                    best = ob;
+                    best_v = ov;
+                }
+            }
+        }
+        if (yy == 0 && wr) {
+            const float r_row = (x0 + xo < nX) ? a.rstd[modoff + x0 + xo] : 0.f;
+            const float lse2 = m_run + __log2f(s);
+            const bool tok = own_tgt >= 0 && own_tgt < nY;
+            const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
+            if (x0 + xo < nX) {
+                const long long t = modoff + x0 + xo;
+                a.lse[t] = lse2 * kLn2;
+                a.rowloss[t] = rl;
+                if (MODE == EVAL && a.top1) a.top1[t] = best_v;
+                if (MODE == LOCAL && a.rowrec) {
+                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), r_row * tau_k * a.inv_T};
+                    *(f32x4*)(a.rowrec + 4 * t) = rec4;
+                }
+            }
+            sbuf[xo] = 1.f / s;
+        }
+    }
+    if (MODE == LOCAL) {
+        __syncthreads();
+        const int xg = x0 + ex;
+        const bool xok = xg < nX;
+        const float rx = xok ? a.rstd[modoff + xg] : 0.f;
+        const int tgt = xok ? a.targets[modoff + xg] : -1;
+        const bool tok = tgt >= 0 && tgt < nY;
+        const float inv_s = sbuf[ex];
+
+        const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
+        const bf16* wrow = Rk + (long long)(tok ? tgt : 0) * d;
+        const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
+        float* dgp = want_dg ? a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d
+                             : nullptr;
+        // sweep 1: acc <- e = (acc / s - R_y) / T, so that dhhat = tau e, and the
+        // row sums of e * g * n (n = r h): the RMSNorm backward's mean(dn * n) =
+        // tau sum / d and the token's share of d loss / d tau
+        float cp = 0.f;
+#pragma unroll
+        for (int b = 0; b < G::NB; ++b) {
+            const int j = js + 16 * b + 4 * eg;
+            const u16x4 hv = *(const u16x4*)(hrow + j);
+            const u16x4 wv = *(const u16x4*)(wrow + j);
+            const u16x4 gv = *(const u16x4*)(gk + j);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float wy = tok ? bf16_bits_to_f32(wv[e]) : 0.f;
+                const float ev = (acc[b][e] * inv_s - wy) * a.inv_T;
+                cp += bf16_bits_to_f32(gv[e]) * ev * (rx * bf16_bits_to_f32(hv[e]));
+                acc[b][e] = ev;
+            }
+        }
+        cp += __shfl_xor(cp, 16, 64);
+        cp += __shfl_xor(cp, 32, 64);
+        if (eg == 0) cbuf[w * XR + ex] = cp;
+        __syncthreads();
+        float csum = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + ex];
+        const float cmean = tau_k * csum / (float)d;
+        if (a.rowdtau && w == 0 && eg == 0 && xok) a.rowdtau[modoff + xg] = tok ? csum : 0.f;
+
+        // sweep 2: dh = r (dn - c n)
+        if (xok) {
+            bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b) {
+                const int j = js + 16 * b + 4 * eg;
+                const u16x4 hv = *(const u16x4*)(hrow + j);
+                const u16x4 gv = *(const u16x4*)(gk + j);
+                bf16x4 o;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float n = rx * bf16_bits_to_f32(hv[e]);
+                    o[e] = (bf16)(rx * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][e] - cmean * n));
+                }
+                *(bf16x4*)(dhrow + j) = o;
+            }
+        }
+        // sweep 3, for a module that trains its gain: the tile's partial sums
+        // of dhhat * n = tau e * n over its 16 rows
+        if (want_dg) {
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b) {
+                const int j = js + 16 * b + 4 * eg;
+                const u16x4 hv = *(const u16x4*)(hrow + j);  // rx = 0 masks rows past the end
+                f32x4 pv;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) pv[e] = row16_sum(tau_k * acc[b][e] * (rx * bf16_bits_to_f32(hv[e])));
+                if (ex == 0) *(f32x4*)(dgp + j) = pv;
+            }
+        }
+    }
+    if (!LL) {
+        // bias gradient of the stationary readout rows: sum over the 16 lanes of the row
+        const float db = row16_sum(db_part);
+        if (a.dbias && yy == 0 && wr && x0 + xo < nX) a.dbias[(long long)k * a.V + x0 + xo] = db * a.inv_T;
+    }
+    if (MODE == RGRAD) {
+        const int v = x0 + ex;
+        if (v < nX) {
+            float* dR = (k == a.K - 1) ? a.dWt : a.dWh + (long long)k * a.V * d;
+            float* dwrow = dR + (long long)v * d;
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b) *(f32x4*)(dwrow + js + 16 * b + 4 * eg) = acc[b];
+        }
+    }
+}
+
+template <int MODE, int DS, bool EXT>
+hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
+    const bool ll = MODE == LOCAL || MODE == EVAL;
+    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
+                   : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
+    hipLaunchKernelGGL((k_fused_wide<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int MODE, bool EXT>
+hipError_t launch_mode(const FusedArgs& a, int nmod, hipStream_t s) {
+    switch (a.d) {
+        case 2560: return launch_ds<MODE, 320, EXT>(a, nmod, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool mfma_wide_supported(int dtype, int d) { return dtype == 0 && d == 2560; }
+
+hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, hipStream_t s) {
+    return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
+}
+hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s) { return launch_mode<EVAL, true>(a, 0, s); }
+hipError_t launch_readout_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_mode<RGRAD, false>(a, nmod, s);
+}
+hipError_t launch_bias_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_mode<BGRAD, false>(a, nmod, s);
+}
+
+}  // namespace solo

@@ -24,7 +24,8 @@ bool flag_ok(int f) { return f == 0 || f == 1; }
 
 // What one call launches, and where its workspace pieces sit.
 struct Plan {
-    bool mfma = false;
+    bool mfma = false;         // matrix-core family (either tiling)
+    bool wide = false;         // the 16-row wide tiling of the matrix-core family (d = 2560)
     bool eval = false;
     bool ext = false;          // local-loss variant with per-chunk biases
     int dg_mode = 0;           // 0 none, 1 terminal only, 2 every module
@@ -44,7 +45,8 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
         !flag_ok(a.heads_train_readout))
         return false;
     const int K = a.K, T = a.T, d = a.d;
-    P->mfma = solo::mfma_supported(a.dtype, d);
+    P->wide = solo::mfma_wide_supported(a.dtype, d);
+    P->mfma = solo::mfma_supported(a.dtype, d) || P->wide;
     P->eval = eval;
     const size_t kt = (size_t)K * T;
     size_t off = 0;
@@ -82,7 +84,7 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
     P->ext = a.bias != nullptr;
     P->dg_mode = a.gain_per_module ? 2 : (fdw ? 1 : 0);
     P->slots = P->dg_mode == 2 ? K : (P->dg_mode == 1 ? 1 : 0);
-    const int rows = P->mfma ? solo::kMfmaRows : solo::kValuRows;
+    const int rows = P->wide ? solo::kMfmaWideRows : (P->mfma ? solo::kMfmaRows : solo::kValuRows);
     P->ntiles = (T + rows - 1) / rows;
     const bool second = P->rg_hi > P->rg_lo || P->bg_hi > P->bg_lo;
     if (P->mfma && second) {
@@ -192,9 +194,13 @@ int run(const solo_readout_args& x, bool eval) {
         return SOLO_ERR_HIP;
     hipError_t e;
     if (eval)
-        e = P.mfma ? solo::launch_exit_eval_mfma(a, s) : solo::launch_exit_eval_valu(dt, a, s);
+        e = P.wide   ? solo::launch_exit_eval_mfma_wide(a, s)
+            : P.mfma ? solo::launch_exit_eval_mfma(a, s)
+                     : solo::launch_exit_eval_valu(dt, a, s);
     else
-        e = P.mfma ? solo::launch_local_loss_mfma(a, P.ext, s) : solo::launch_local_loss_valu(dt, a, s);
+        e = P.wide   ? solo::launch_local_loss_mfma_wide(a, P.ext, s)
+            : P.mfma ? solo::launch_local_loss_mfma(a, P.ext, s)
+                     : solo::launch_local_loss_valu(dt, a, s);
     if (e != hipSuccess || !mark(1)) return SOLO_ERR_HIP;
     if (solo::launch_module_sum(a.rowloss, x.losses, K, T, 1.0 / (double)T, s) != hipSuccess) return SOLO_ERR_HIP;
     if (a.rowdtau && solo::launch_module_sum(a.rowdtau, x.dtau, K, T, 1.0, s) != hipSuccess) return SOLO_ERR_HIP;
@@ -206,14 +212,18 @@ int run(const solo_readout_args& x, bool eval) {
     if (!eval && P.rg_hi > P.rg_lo) {
         a.m0 = P.rg_lo;
         const int n = P.rg_hi - P.rg_lo;
-        e = P.mfma ? solo::launch_readout_grad_mfma(a, n, s) : solo::launch_readout_grad_valu(dt, a, n, s);
+        e = P.wide   ? solo::launch_readout_grad_mfma_wide(a, n, s)
+            : P.mfma ? solo::launch_readout_grad_mfma(a, n, s)
+                     : solo::launch_readout_grad_valu(dt, a, n, s);
         if (e != hipSuccess) return SOLO_ERR_HIP;
     }
     if (!mark(3)) return SOLO_ERR_HIP;
     if (!eval && P.bg_hi > P.bg_lo) {
         a.m0 = P.bg_lo;
         const int n = P.bg_hi - P.bg_lo;
-        e = P.mfma ? solo::launch_bias_grad_mfma(a, n, s) : solo::launch_bias_grad_valu(dt, a, n, s);
+        e = P.wide   ? solo::launch_bias_grad_mfma_wide(a, n, s)
+            : P.mfma ? solo::launch_bias_grad_mfma(a, n, s)
+                     : solo::launch_bias_grad_valu(dt, a, n, s);
         if (e != hipSuccess) return SOLO_ERR_HIP;
     }
     if (!mark(4)) return SOLO_ERR_HIP;
@@ -284,6 +294,7 @@ size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int fi
 
 const char* solo_readout_kernel_family(int K, int T, int d, int V, int dtype) {
     if ((dtype != SOLO_BF16 && dtype != SOLO_F32) || !shape_ok(K, T, d, V)) return "invalid";
+    if (solo::mfma_wide_supported(dtype, d)) return "mfma_wide";
     return solo::mfma_supported(dtype, d) ? "mfma" : "valu";
 }
 

@@ -51,6 +51,7 @@ struct FusedArgs {
 
 // Tile sizes of the two kernel families (the workspace depends on them).
 constexpr int kMfmaRows = 32;      // stationary rows per workgroup (matrix-core kernels)
+constexpr int kMfmaWideRows = 16;  // stationary rows per workgroup (wide matrix-core kernels, d = 2560)
 constexpr int kValuRows = 8;       // stationary rows per workgroup (vector-ALU kernels)
 
 // small kernels (k_small.hip)
@@ -70,6 +71,12 @@ hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s);
 hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s);
 hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_bias_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
+// the wide matrix-core kernels (k_mfma_wide.hip): d = 2560
+bool mfma_wide_supported(int dtype, int d);
+hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, hipStream_t s);
+hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s);
+hipError_t launch_readout_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s);
+hipError_t launch_bias_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s);
 hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, hipStream_t s);
 hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);

@@ -16,6 +16,7 @@
 #include <vector>
 
 #include "mfma_layout.h"
+#include "mfma_layout_wide.h"
 
 using namespace solo::layout;
 
@@ -103,6 +104,70 @@ int report() {
     return e;
 }
 
+
+// The wide layout (mfma_layout_wide.h): staged register -> LDS writes of one
+// wave slice, the row-wise reads of the 16x16x32 logit product and the
+// transposing reads of the 16x16x16 second product.
+template <int DS>
+int check_wide(int& conflicts_row, int& conflicts_tr, int& conflicts_wr) {
+    namespace W = solo::layoutw;
+    using G = W::Geo<DS>;
+    int errors = 0;
+    conflicts_row = conflicts_tr = conflicts_wr = 0;
+    std::map<int, std::pair<int, int>> lds;  // LDS byte -> (row, column within the slice)
+    for (int q = 0; q < G::NI; ++q) {
+        int addr[64];
+        for (int p = 0; p < 64; ++p) {
+            const int row = W::stage_row<DS>(q, p), gran = W::stage_gran<DS>(q, p);
+            const int a = W::stage_dst<DS>(q, p);
+            addr[p] = a;
+            if (row < 0 || row >= 16 || a < 0 || a + 16 > G::SLICE) ++errors;
+            for (int e = 0; e < 8; ++e) {
+                if (lds.count(a + 2 * e)) ++errors;
+                lds[a + 2 * e] = {row, 8 * gran + e};
+            }
+        }
+        conflicts_wr += conflicts(addr, 16, 8, 32);
+    }
+    if ((int)lds.size() != 16 * DS) ++errors;
+    for (int kk = 0; kk < DS / 32; ++kk) {
+        int addr[64];
+        for (int l = 0; l < 64; ++l) {
+            addr[l] = W::rowread_off<DS>(l, kk);
+            for (int e = 0; e < 8; ++e) {
+                auto it = lds.find(addr[l] + 2 * e);
+                std::pair<int, int> want{l & 15, 32 * kk + 8 * (l >> 4) + e};
+                if (it == lds.end() || it->second != want) ++errors;
+            }
+        }
+        conflicts_row += conflicts(addr, 16, 8, 32);
+    }
+    for (int b = 0; b < DS / 16; ++b) {
+        int addr[64];
+        for (int l = 0; l < 64; ++l) addr[l] = W::trread_off<DS>(l, b);
+        conflicts_tr += conflicts(addr, 8, 32, 64);
+        for (int l = 0; l < 64; ++l) {
+            const int grp = l / 16, i = l % 16;
+            for (int e = 0; e < 4; ++e) {
+                const int src = grp * 16 + 4 * e + i / 4;
+                auto it = lds.find(addr[src] + 2 * (i % 4));
+                std::pair<int, int> want{4 * grp + e, 16 * b + i};  // A[m = column][k = row] of the 16x16x16 product
+                if (it == lds.end() || it->second != want) ++errors;
+            }
+        }
+    }
+    return errors;
+}
+
+template <int DS>
+int report_wide() {
+    int cr = 0, ct = 0, cw = 0;
+    const int e = check_wide<DS>(cr, ct, cw);
+    std::printf("WIDE DS=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d write_conflicts=%d\n", DS,
+                solo::layoutw::Geo<DS>::SLICE, e, cr, ct, cw);
+    return e;
+}
+
 int main() {
     int e = 0;
     e += report<32>();
@@ -117,5 +182,8 @@ int main() {
     e += report<256, 4>();
     e += report<384, 4>();
     e += report<512, 4>();
+    // the wide layout: 8 waves of d / 8 columns; 320 is the shipped width (d = 2560)
+    e += report_wide<320>();
+    e += report_wide<384>();
     return e == 0 ? 0 : 1;
 }

@@ -81,7 +81,9 @@ def test_kernel_family():
     assert B.kernel_family(4, 16384, 2048, 32000, B.SOLO_BF16) == "mfma"
     assert B.kernel_family(4, 8192, 1024, 32000, B.SOLO_BF16) == "mfma"
     assert B.kernel_family(2, 256, 64, 512, B.SOLO_F32) == "valu"
-    assert B.kernel_family(8, 16384, 2560, 32000, B.SOLO_BF16) == "valu"
+    assert B.kernel_family(8, 16384, 2560, 32000, B.SOLO_BF16) == "mfma_wide"
+    assert B.kernel_family(8, 16384, 3072, 32000, B.SOLO_BF16) == "valu"
+    assert B.kernel_family(8, 16384, 2560, 32000, B.SOLO_F32) == "valu"
     assert B.kernel_family(1, 1, 72, 3, B.SOLO_BF16) == "valu"
     assert B.kernel_family(0, 1, 64, 3, B.SOLO_BF16) == "invalid"
 

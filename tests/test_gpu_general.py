@@ -36,6 +36,10 @@ CASES = [
      dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
     ("mfma_T1_all", "340m", dict(K=2, T=1, d=256, V=60), ALL,
      dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
+    ("wide_d2560_all", "2b", dict(K=3, T=37, d=2560, V=300), ALL,
+     dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
+    ("wide_d2560_shared_copy_bias", "2b", dict(K=3, T=20, d=2560, V=70),
+     dict(wbar="shared", tau=True, bias=True), dict(final_module_dW=True, want_dtau=True, want_dbias=True)),
     ("valu_f32_all", "tiny", dict(K=3, T=37, d=24, V=45), ALL,
      dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
     ("valu_f32_shared_copy", "tiny", dict(K=2, T=20, d=64, V=33), dict(wbar="shared", tau=True, bias=True),
@@ -148,8 +152,9 @@ def test_general_headline_options_match_headline_entry_point():
         np.testing.assert_array_equal(a[key], b[key])
 
 
-def test_general_bitwise_determinism():
-    x = make_extras(make_inputs("1b", seed=23, K=3, T=64, d=2048, V=400), 23, **ALL)
+@pytest.mark.parametrize("cfg,d", [("1b", 2048), ("2b", 2560)])
+def test_general_bitwise_determinism(cfg, d):
+    x = make_extras(make_inputs(cfg, seed=23, K=3, T=64, d=d, V=400), 23, **ALL)
     flags = dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)
     a = run_general(x, flags)
     b = run_general(x, flags)
@@ -180,6 +185,7 @@ EVAL_CASES = [
     ("mfma_d2048", "1b", dict(K=3, T=65, d=2048, V=515), ALL),
     ("mfma_d256_plain", "340m", dict(K=2, T=70, d=256, V=300), dict()),
     ("mfma_d1024_shared", "340m", dict(K=3, T=40, d=1024, V=1000), dict(wbar="shared", tau=True)),
+    ("wide_d2560", "2b", dict(K=3, T=37, d=2560, V=300), ALL),
     ("valu_f32", "tiny", dict(K=3, T=37, d=24, V=45), ALL),
     ("valu_bf16_d72", "340m", dict(K=2, T=10, d=72, V=50), ALL),
 ]

@@ -26,7 +26,11 @@ CASES = [
     ("mfma_d2048_frozen_only", "1b", dict(K=3, T=64, d=2048, V=320), False),
     ("mfma_large_vocab_hot", "large_vocab", dict(K=2, T=256, d=2048, V=4099), True),
     ("mfma_2b_scaled", "2b", dict(K=3, T=50, d=2048, V=100), True),
-    ("valu_d2560", "2b", dict(K=2, T=40, d=2560, V=300), True),
+    ("wide_d2560", "2b", dict(K=2, T=40, d=2560, V=300), True),
+    ("wide_d2560_ragged", "2b", dict(K=3, T=37, d=2560, V=515), True),
+    ("wide_d2560_frozen_only", "2b", dict(K=2, T=33, d=2560, V=129), False),
+    ("wide_d2560_V1", "2b", dict(K=2, T=20, d=2560, V=1), True),
+    ("wide_d2560_T1", "2b", dict(K=2, T=1, d=2560, V=77), True),
     ("valu_d72", "340m", dict(K=2, T=10, d=72, V=50), True),
     ("mfma_V1", "340m", dict(K=2, T=40, d=256, V=1), True),
     ("mfma_V2", "340m", dict(K=2, T=40, d=256, V=2), True),

@@ -28,3 +28,12 @@ def test_layout_reads_match_stream(tmp_path):
         assert int(m.group(4)) == 0, key
         if m.group(3) == "1":  # padded layouts (DS = 128, 256, 512): transposing reads conflict-free
             assert int(m.group(6)) == 0, key
+    # the wide layout: every staged write lands once and every read returns its operand;
+    # at the shipped width (320 columns per wave) all three access patterns are conflict-free
+    wide = {int(m.group(1)): m for m in re.finditer(
+        r"WIDE DS=(\d+) slice=\d+ errors=(\d+) row_conflicts=(\d+) tr_conflicts=(\d+) write_conflicts=(\d+)",
+        r.stdout)}
+    assert sorted(wide) == [320, 384]
+    for ds, m in wide.items():
+        assert int(m.group(2)) == 0, ds
+    assert [int(wide[320].group(i)) for i in (3, 4, 5)] == [0, 0, 0]
