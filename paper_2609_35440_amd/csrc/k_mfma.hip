@@ -48,14 +48,23 @@ using namespace mfma;
 
 constexpr int NW = layout::NW;  // waves per workgroup
 constexpr int NTHR = NW * 64;
-constexpr int XR = kMfmaRows;  // stationary rows per workgroup (32)
 constexpr int YC = layout::YC;  // streamed rows per chunk
 constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: conflict-free 16 B writes
 
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
 
+// Stationary rows per workgroup: 64 while the accumulator (64 rows x d/8
+// columns) and the stationary operand fit the register file (d <= 1024),
+// 32 otherwise.  The readout streamed per flop halves with the taller tile.
+template <int DS>
+constexpr int rows_of() { return DS <= 128 ? 64 : 32; }
+
 template <int DS>
 struct Geo : layout::Geo<DS> {
+    static constexpr int XR = rows_of<DS>();           // stationary rows per workgroup
+    static constexpr int NXB = XR / 16;                // 16-row blocks of the logit product
+    static constexpr int NR = XR / 32;                 // rows per lane in the elementwise step = 32-row
+                                                       // halves of the second product
     static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
     static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
     static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
@@ -67,12 +76,14 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
     return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
 }
 
-// MODE LOCAL / EVAL: grid (ceil(T/32), K); module k = blockIdx.y.
-// MODE RGRAD / BGRAD: grid (ceil(V/32), nmod); module k = m0 + blockIdx.y.
+// MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
+// MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
 // EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     using G = Geo<DS>;
+    constexpr int XR = G::XR;
+    constexpr int NR = G::NR;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
     constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
@@ -115,18 +126,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     LDS_AS char* sliceA = (LDS_AS char*)(LDS_AS void*)ybufA + w * G::SLICE;
     LDS_AS char* sliceB = (LDS_AS char*)(LDS_AS void*)ybufB + w * G::SLICE;
 
-    // per-lane scalars of the rows this wave finishes in the elementwise step
-    const int xo = 4 * w + (lane >> 4);   // stationary row (0..31) owned in the elementwise step
-    const int yy = lane & 15;             // streamed row within the chunk
-    float own_r2 = 0.f;                   // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
-    int own_tgt = -1;                     // LL: target of row xo
-    if (LL && x0 + xo < nX) {
-        own_r2 = a.rstd[modoff + x0 + xo] * tau_k * kLog2e;
-        own_tgt = a.targets[modoff + x0 + xo];
+    // per-lane scalars of the rows this wave finishes in the elementwise step:
+    // stationary rows xo[r] = 4 w + lane/16 + 32 r, streamed row yy of the chunk
+    int xo[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) xo[r] = 4 * w + (lane >> 4) + 32 * r;
+    const int yy = lane & 15;
+    float own_r2[NR];  // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
+    int own_tgt[NR];   // LL: target of row xo
+    float bx2[NR];     // readout-/bias-gradient passes: bias of the stationary readout row, base 2
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        own_r2[r] = 0.f;
+        own_tgt[r] = -1;
+        bx2[r] = 0.f;
+        if (LL && x0 + xo[r] < nX) {
+            own_r2[r] = a.rstd[modoff + x0 + xo[r]] * tau_k * kLog2e;
+            own_tgt[r] = a.targets[modoff + x0 + xo[r]];
+        }
+        if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
     }
-    // readout-/bias-gradient passes: bias of the stationary readout row, base 2
-    float bx2 = 0.f;
-    if (!LL && a.bias && x0 + xo < nX) bx2 = a.bias[(long long)k * a.V + x0 + xo] * kLog2e;
     const bool has_bias = a.bias != nullptr;
 
     ChunkStream<DS> stream;
@@ -154,13 +173,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     // stationary operand (local loss and exit evaluation: times the gain,
     // rounded once): B of the 16x16x32 logit product, lane holds
     // X[x0 + 16 xb + lane%16][js + 32 kk + 8 (lane/16) .. +7]
-    bf16x8 xr[2][G::NK];
+    bf16x8 xr[G::NXB][G::NK];
 #pragma unroll
     for (int kk = 0; kk < G::NK; ++kk) {
         const int j0 = js + 32 * kk + 8 * (lane >> 4);
         const bf16x8 gv = *(const bf16x8*)(gk + j0);
 #pragma unroll
-        for (int xb = 0; xb < 2; ++xb) {
+        for (int xb = 0; xb < G::NXB; ++xb) {
             const int xrow = x0 + 16 * xb + (lane & 15);
             bf16x8 xv;
             if (xrow < nX) {
@@ -178,17 +197,27 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
     }
 
-    f32x16 acc[PC ? G::NB : 1];
+    // accumulator: 32-column block b of this wave's slice, 32-row half h of the tile
+    f32x16 acc[PC ? G::NB : 1][NR];
 #pragma unroll
     for (int b = 0; b < (PC ? G::NB : 1); ++b)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[b][i] = 0.f;
+        for (int h = 0; h < NR; ++h)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[b][h][i] = 0.f;
 
-    // online softmax state (LL, base 2), per lane: row xo, streamed column yy
-    float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
-    float best = -INFINITY;               // EVAL: largest logit seen by this lane, and its column
-    int best_v = -1;
-    float db_part = 0.f;                  // RGRAD / BGRAD: sum_t (p - onehot) for row xo
+    // online softmax state (LL, base 2), per lane and row r: row xo[r], streamed column yy
+    float m_run[NR], s_part[NR], zy_part[NR];
+    float best[NR];   // EVAL: largest logit seen by this lane, and its column
+    int best_v[NR];
+    float db_part[NR];  // RGRAD / BGRAD: sum_t (p - onehot) for row xo[r]
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        m_run[r] = -INFINITY;
+        s_part[r] = zy_part[r] = db_part[r] = 0.f;
+        best[r] = -INFINITY;
+        best_v[r] = -1;
+    }
 
     // per-lane parts of the LDS addresses; the unrolled loops add 64 * kk or 64 * b
     const int a_off = layout::rowread_off<DS>(lane);
@@ -213,11 +242,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
         for (int kk = 0; kk < RA; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
         if (more) issue_side(y0 + YC, side_nxt);
-        f32x4 S0 = {0.f, 0.f, 0.f, 0.f}, S1 = {0.f, 0.f, 0.f, 0.f};
+        f32x4 S[G::NXB];
+#pragma unroll
+        for (int xb = 0; xb < G::NXB; ++xb) S[xb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
-            S0 = mfma16(ay[kk % RA], xr[0][kk], S0);
-            S1 = mfma16(ay[kk % RA], xr[1][kk], S1);
+#pragma unroll
+            for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay[kk % RA], xr[xb][kk], S[xb]);
             if (kk + RA < G::NK) ay[kk % RA] = *(LDS_AS bf16x8*)(cur + a_off + 64 * (kk + RA));
             if (kk < kDmaA) {
                 if (more) stream.issue_one(nrs, d, nxt, kk);
@@ -225,66 +256,75 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
         }
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
-        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
-        *(f32x4*)(part + (w * XR + 16 + (lane & 15)) * PP + 4 * (lane >> 4)) = S1;
+#pragma unroll
+        for (int xb = 0; xb < G::NXB; ++xb)
+            *(f32x4*)(part + (w * XR + 16 * xb + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
         lds_barrier();
 
-        // ---- elementwise step for rows xo = 4w .. 4w+3 (lane: row xo, column yy)
+        // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
+        const int yg = y0 + yy;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
         float q[NW];
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + yy];
+        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo[r]) * PP + yy];
         static_assert(NW == 8, "partial-sum tree");
         const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
-        const int yg = y0 + yy;
         float gval = 0.f;
         if (LL) {
             // columns past the end of the vocabulary get z = -inf (an additive
             // mask rather than a branch, so the partial reads stay unconditional)
             float ymask = (yg < nY) ? 0.f : -INFINITY;
             if (BZ && has_bias) ymask += side[yy] * kLog2e;
-            const float zc = __builtin_fmaf(sxy, own_r2, ymask);
+            const float zc = __builtin_fmaf(sxy, own_r2[r], ymask);
             float alpha = 1.f;
-            if (__builtin_expect(__any(zc > m_run + kLazyThresh2), 0)) {  // wave-uniform
+            if (__builtin_expect(__any(zc > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
                 const float cmax = row16_max(zc);
-                if (cmax > m_run + kLazyThresh2) {
-                    alpha = __builtin_amdgcn_exp2f(m_run - cmax);
-                    s_part *= alpha;
-                    m_run = cmax;
+                if (cmax > m_run[r] + kLazyThresh2) {
+                    alpha = __builtin_amdgcn_exp2f(m_run[r] - cmax);
+                    s_part[r] *= alpha;
+                    m_run[r] = cmax;
                 }
             }
-            const float p = __builtin_amdgcn_exp2f(zc - m_run);
-            s_part += p;
-            if (yg == own_tgt) zy_part = zc;
-            if (MODE == EVAL && zc > best) {  // strict: the first (lowest) column keeps a tie
-                best = zc;
-                best_v = yg;
+            const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
+            s_part[r] += p;
+            if (yg == own_tgt[r]) zy_part[r] = zc;
+            if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
+                best[r] = zc;
+                best_v[r] = yg;
             }
             gval = p;
-            if (MODE == LOCAL) abuf[xo] = alpha;  // the 16 lanes of a row store the same value
+            if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
         } else {
             // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
             // the end of the module read as zeros and are masked
             const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2 - r4[0]));
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
             // (a padded token's zero record would match readout row 0 as its target)
-            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f) : 0.f;
+            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
             gval = dlt * r4[3];
-            db_part += dlt;
+            db_part[r] += dlt;
         }
-        if (PC) gbuf[xo * YC + yy] = (bf16)gval;
+        if (PC) gbuf[xo[r] * YC + yy] = (bf16)gval;
+        }
         if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
         lds_barrier();
 
         if (PC) {
             // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
-            const bf16x8 gfrag = *(bf16x8*)(gbuf + (lane & 31) * YC + 8 * (lane >> 5));
+            bf16x8 gfrag[NR];
+#pragma unroll
+            for (int h = 0; h < NR; ++h) gfrag[h] = *(bf16x8*)(gbuf + (32 * h + (lane & 31)) * YC + 8 * (lane >> 5));
             if (MODE == LOCAL) {
-                const float al = abuf[lane & 31];
-                if (__any(al != 1.f)) {
 #pragma unroll
-                    for (int b = 0; b < G::NB; ++b)
+                for (int h = 0; h < NR; ++h) {
+                    const float al = abuf[32 * h + (lane & 31)];
+                    if (__any(al != 1.f)) {
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) acc[b][i] *= al;
+                        for (int b = 0; b < G::NB; ++b)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) acc[b][h][i] *= al;
+                    }
                 }
             }
             bf16x4 tlo[G::NB], thi[G::NB];
@@ -298,7 +338,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 bf16x8 at;
                 at[0] = tlo[b][0]; at[1] = tlo[b][1]; at[2] = tlo[b][2]; at[3] = tlo[b][3];
                 at[4] = thi[b][0]; at[5] = thi[b][1]; at[6] = thi[b][2]; at[7] = thi[b][3];
-                acc[PC ? b : 0] = mfma32(at, gfrag, acc[PC ? b : 0]);
+#pragma unroll
+                for (int h = 0; h < NR; ++h) acc[PC ? b : 0][h] = mfma32(at, gfrag[h], acc[PC ? b : 0][h]);
             }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -311,128 +352,145 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (c + 1 < nchunks) step(sliceB, sliceA_u, (LDS_AS float*)(LDS_AS void*)recB, recA_u, c + 1);
     }
 
-    // ---- epilogues.  acc[b] lane layout: x = lane%32,
+    // ---- epilogues.  acc[b][h] lane layout: x = 32 h + lane%32,
     //      j = js + 32 b + 8 (i/4) + 4 (lane/32) + i%4 for i = 0..15
     const int ex = lane & 31;
     const int ehh = lane >> 5;
     if (LL) {
-        // finish the online softmax of rows 4w..4w+3
-        const float s = row16_sum(s_part);
-        const float zy = row16_sum(zy_part);
-        if (MODE == EVAL) {
-            // argmax over the 16 lanes of the row: larger logit, then lower column
+        // finish the online softmax of rows xo[r]
 #pragma unroll
-            for (int off = 1; off < 16; off <<= 1) {
-                const float ob = __shfl_xor(best, off, 64);
-                const int ov = __shfl_xor(best_v, off, 64);
-                if (ob > best || (ob == best && (unsigned)ov < (unsigned)best_v)) {
-                    best = ob;
-                    best_v = ov;
+        for (int r = 0; r < NR; ++r) {
+            const float s = row16_sum(s_part[r]);
+            const float zy = row16_sum(zy_part[r]);
+            float bst = best[r];
+            int bv = best_v[r];
+            if (MODE == EVAL) {
+                // argmax over the 16 lanes of the row: larger logit, then lower column
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    const float ob = __shfl_xor(bst, off, 64);
+                    const int ov = __shfl_xor(bv, off, 64);
+                    if (ob > bst || (ob == bst && (unsigned)ov < (unsigned)bv)) {
+                        bst = ob;
+                        bv = ov;
+                    }
                 }
             }
-        }
-        if (yy == 0) {
-            const float r_row = (x0 + xo < nX) ? a.rstd[modoff + x0 + xo] : 0.f;
-            const float lse2 = m_run + __log2f(s);
-            const bool tok = own_tgt >= 0 && own_tgt < nY;
-            const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
-            if (x0 + xo < nX) {
-                const long long t = modoff + x0 + xo;
-                a.lse[t] = lse2 * kLn2;
-                a.rowloss[t] = rl;
-                if (MODE == EVAL && a.top1) a.top1[t] = best_v;
-                if (MODE == LOCAL && a.rowrec) {
-                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), r_row * tau_k * a.inv_T};
-                    *(f32x4*)(a.rowrec + 4 * t) = rec4;
+            if (yy == 0) {
+                const int xr_ = x0 + xo[r];
+                const float r_row = (xr_ < nX) ? a.rstd[modoff + xr_] : 0.f;
+                const float lse2 = m_run[r] + __log2f(s);
+                const bool tok = own_tgt[r] >= 0 && own_tgt[r] < nY;
+                const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
+                if (xr_ < nX) {
+                    const long long t = modoff + xr_;
+                    a.lse[t] = lse2 * kLn2;
+                    a.rowloss[t] = rl;
+                    if (MODE == EVAL && a.top1) a.top1[t] = bv;
+                    if (MODE == LOCAL && a.rowrec) {
+                        f32x4 rec4 = {lse2, own_r2[r], __int_as_float(own_tgt[r]), r_row * tau_k * a.inv_T};
+                        *(f32x4*)(a.rowrec + 4 * t) = rec4;
+                    }
                 }
+                sbuf[xo[r]] = 1.f / s;
             }
-            sbuf[xo] = 1.f / s;
         }
     }
     if (MODE == LOCAL) {
         __syncthreads();
-        const int xg = x0 + ex;
-        const bool xok = xg < nX;
-        const float rx = xok ? a.rstd[modoff + xg] : 0.f;
-        const int tgt = xok ? a.targets[modoff + xg] : -1;
-        const bool tok = tgt >= 0 && tgt < nY;
-        const float inv_s = sbuf[ex];
-
-        const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
-        const bf16* wrow = Rk + (long long)(tok ? tgt : 0) * d;
         const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
         float* dgp = want_dg ? a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d
                              : nullptr;
+        bool xok[NR], tok[NR];
+        float rx[NR];
+        const bf16* hrow[NR];
         // sweep 1: acc <- e = (acc / s - R_y) / T, so that dhhat = tau e, and the
         // row sums of e * g * n (n = r h).  That row sum is both the RMSNorm
         // backward's mean(dn * n) = tau sum / d and the token's share of
         // d loss / d tau = sum_v delta_v u_v = <sum_v delta_v R_v, g * n>.
-        float cp = 0.f;
 #pragma unroll
-        for (int b = 0; b < (PC ? G::NB : 1); ++b) {
-#pragma unroll
-            for (int i4 = 0; i4 < 4; ++i4) {
-                const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                // unconditional loads (the row pointers are clamped to row 0), masked
-                // afterwards: no control flow inside the sweep
-                const u16x4 hv = *(const u16x4*)(hrow + j);
-                const u16x4 wv = *(const u16x4*)(wrow + j);
-                const u16x4 gv = *(const u16x4*)(gk + j);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float wy = tok ? bf16_bits_to_f32(wv[e]) : 0.f;
-                    const float ev = (acc[b][4 * i4 + e] * inv_s - wy) * a.inv_T;
-                    cp += bf16_bits_to_f32(gv[e]) * ev * (rx * bf16_bits_to_f32(hv[e]));
-                    acc[b][4 * i4 + e] = ev;
-                }
-            }
-            __builtin_amdgcn_sched_barrier(0);  // one block's loads at a time
-        }
-        cp += __shfl_xor(cp, 32, 64);
-        if (ehh == 0) cbuf[w * XR + ex] = cp;
-        __syncthreads();
-        float csum = 0.f;
-#pragma unroll
-        for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + ex];
-        const float cmean = tau_k * csum / (float)d;
-        if (a.rowdtau && w == 0 && ehh == 0 && xok) a.rowdtau[modoff + xg] = tok ? csum : 0.f;
-
-        // sweep 2: dh = r (dn - c n)
-        if (xok) {
-            bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
+        for (int h = 0; h < NR; ++h) {
+            const int xg = x0 + 32 * h + ex;
+            xok[h] = xg < nX;
+            rx[h] = xok[h] ? a.rstd[modoff + xg] : 0.f;
+            const int tgt = xok[h] ? a.targets[modoff + xg] : -1;
+            tok[h] = tgt >= 0 && tgt < nY;
+            const float inv_s = sbuf[32 * h + ex];
+            hrow[h] = hk + (long long)(xok[h] ? xg : 0) * d;
+            const bf16* wrow = Rk + (long long)(tok[h] ? tgt : 0) * d;
+            float cp = 0.f;
 #pragma unroll
             for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
                 for (int i4 = 0; i4 < 4; ++i4) {
                     const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                    const u16x4 hv = *(const u16x4*)(hrow + j);
+                    // unconditional loads (the row pointers are clamped to row 0), masked
+                    // afterwards: no control flow inside the sweep
+                    const u16x4 hv = *(const u16x4*)(hrow[h] + j);
+                    const u16x4 wv = *(const u16x4*)(wrow + j);
                     const u16x4 gv = *(const u16x4*)(gk + j);
-                    bf16x4 o;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float n = rx * bf16_bits_to_f32(hv[e]);
-                        o[e] = (bf16)(rx * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][4 * i4 + e] - cmean * n));
+                        const float wy = tok[h] ? bf16_bits_to_f32(wv[e]) : 0.f;
+                        const float ev = (acc[b][h][4 * i4 + e] * inv_s - wy) * a.inv_T;
+                        cp += bf16_bits_to_f32(gv[e]) * ev * (rx[h] * bf16_bits_to_f32(hv[e]));
+                        acc[b][h][4 * i4 + e] = ev;
                     }
-                    *(bf16x4*)(dhrow + j) = o;
                 }
-                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_sched_barrier(0);  // one block's loads at a time
+            }
+            cp += __shfl_xor(cp, 32, 64);
+            if (ehh == 0) cbuf[w * XR + 32 * h + ex] = cp;
+        }
+        __syncthreads();
+        // sweep 2: dh = r (dn - c n)
+#pragma unroll
+        for (int h = 0; h < NR; ++h) {
+            const int xg = x0 + 32 * h + ex;
+            float csum = 0.f;
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + 32 * h + ex];
+            const float cmean = tau_k * csum / (float)d;
+            if (a.rowdtau && w == 0 && ehh == 0 && xok[h]) a.rowdtau[modoff + xg] = tok[h] ? csum : 0.f;
+            if (xok[h]) {
+                bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
+#pragma unroll
+                for (int b = 0; b < (PC ? G::NB : 1); ++b) {
+#pragma unroll
+                    for (int i4 = 0; i4 < 4; ++i4) {
+                        const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                        const u16x4 hv = *(const u16x4*)(hrow[h] + j);
+                        const u16x4 gv = *(const u16x4*)(gk + j);
+                        bf16x4 o;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float n = rx[h] * bf16_bits_to_f32(hv[e]);
+                            o[e] = (bf16)(rx[h] * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][h][4 * i4 + e] - cmean * n));
+                        }
+                        *(bf16x4*)(dhrow + j) = o;
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
         // sweep 3, for a module that trains its gain: the tile's partial sums
-        // of dhhat * n = tau e * n over its 32 rows (the 16-lane row, then the other row
-        // of the half-wave)
+        // of dhhat * n = tau e * n over its rows (the 16-lane row, the other row
+        // of the half-wave, then the other 32-row half of the tile)
         if (want_dg) {
 #pragma unroll
             for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
                 for (int i4 = 0; i4 < 4; ++i4) {
                     const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                    const u16x4 hv = *(const u16x4*)(hrow + j);  // rx = 0 masks rows past the end
-                    f32x4 pv;
+                    f32x4 pv = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float t = row16_sum(tau_k * acc[b][4 * i4 + e] * (rx * bf16_bits_to_f32(hv[e])));
-                        pv[e] = t + __shfl_xor(t, 16, 64);
+                    for (int h = 0; h < NR; ++h) {
+                        const u16x4 hv = *(const u16x4*)(hrow[h] + j);  // rx = 0 masks rows past the end
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float t = row16_sum(tau_k * acc[b][h][4 * i4 + e] * (rx[h] * bf16_bits_to_f32(hv[e])));
+                            pv[e] += t + __shfl_xor(t, 16, 64);
+                        }
                     }
                     if (ex == 0) *(f32x4*)(dgp + j) = pv;
                 }
@@ -441,24 +499,30 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     }
     if (!LL) {
         // bias gradient of the stationary readout rows: sum over the 16 lanes of the row
-        const float db = row16_sum(db_part);
-        if (a.dbias && yy == 0 && x0 + xo < nX) a.dbias[(long long)k * a.V + x0 + xo] = db * a.inv_T;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const float db = row16_sum(db_part[r]);
+            if (a.dbias && yy == 0 && x0 + xo[r] < nX) a.dbias[(long long)k * a.V + x0 + xo[r]] = db * a.inv_T;
+        }
     }
     if (MODE == RGRAD) {
         // dR_v = D_v
-        const int v = x0 + ex;
-        const bool vok = v < nX;
-        float* dR = (k == a.K - 1) ? a.dWt : a.dWh + (long long)k * a.V * d;
-        float* dwrow = dR + (long long)(vok ? v : 0) * d;
 #pragma unroll
-        for (int b = 0; b < (PC ? G::NB : 1); ++b) {
+        for (int h = 0; h < NR; ++h) {
+            const int v = x0 + 32 * h + ex;
+            const bool vok = v < nX;
+            float* dR = (k == a.K - 1) ? a.dWt : a.dWh + (long long)k * a.V * d;
+            float* dwrow = dR + (long long)(vok ? v : 0) * d;
 #pragma unroll
-            for (int i4 = 0; i4 < 4; ++i4) {
-                const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                f32x4 o;
+            for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) o[e] = acc[b][4 * i4 + e];
-                if (vok) *(f32x4*)(dwrow + j) = o;
+                for (int i4 = 0; i4 < 4; ++i4) {
+                    const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                    f32x4 o;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] = acc[b][h][4 * i4 + e];
+                    if (vok) *(f32x4*)(dwrow + j) = o;
+                }
             }
         }
     }
@@ -467,6 +531,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 template <int MODE, int DS, bool EXT>
 hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
     const bool ll = MODE == LOCAL || MODE == EVAL;
+    constexpr int XR = Geo<DS>::XR;
     dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
                    : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
@@ -491,6 +556,8 @@ hipError_t launch_mode(const FusedArgs& a, int nmod, hipStream_t s) {
 }  // namespace
 
 bool mfma_supported(int dtype, int d) { return dtype == 0 && d % (NW * 32) == 0 && d >= NW * 32 && d <= NW * 256; }
+
+int mfma_rows(int d) { return d <= NW * 128 ? rows_of<128>() : rows_of<256>(); }
 
 hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s) {
     return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);

@@ -84,7 +84,7 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
     P->ext = a.bias != nullptr;
     P->dg_mode = a.gain_per_module ? 2 : (fdw ? 1 : 0);
     P->slots = P->dg_mode == 2 ? K : (P->dg_mode == 1 ? 1 : 0);
-    const int rows = P->wide ? solo::kMfmaWideRows : (P->mfma ? solo::kMfmaRows : solo::kValuRows);
+    const int rows = P->wide ? solo::kMfmaWideRows : (P->mfma ? solo::mfma_rows(d) : solo::kValuRows);
     P->ntiles = (T + rows - 1) / rows;
     const bool second = P->rg_hi > P->rg_lo || P->bg_hi > P->bg_lo;
     if (P->mfma && second) {

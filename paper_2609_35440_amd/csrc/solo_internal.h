@@ -50,7 +50,7 @@ struct FusedArgs {
 };
 
 // Tile sizes of the two kernel families (the workspace depends on them).
-constexpr int kMfmaRows = 32;      // stationary rows per workgroup (matrix-core kernels)
+constexpr int kMfmaRows = 32;      // stationary rows per workgroup of the matrix-core kernels at d > 1024
 constexpr int kMfmaWideRows = 16;  // stationary rows per workgroup (wide matrix-core kernels, d = 2560)
 constexpr int kValuRows = 8;       // stationary rows per workgroup (vector-ALU kernels)
 
@@ -67,6 +67,7 @@ hipError_t launch_dgain_reduce(const float* part, float* dgain, int slots, int n
 // fused passes; `ext` selects the local-loss variant with per-chunk biases,
 // `nmod` is the number of modules of a readout-/bias-gradient launch
 bool mfma_supported(int dtype, int d);
+int mfma_rows(int d);  // stationary rows per workgroup of the matrix-core kernels at width d (64 or 32)
 hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s);
 hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s);
 hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);

@@ -51,11 +51,13 @@ def al(x):
 
 
 def test_workspace_has_no_TV_term():
-    # bf16 matrix-core family: rstd, lse, row_loss (3 K T 4) + per-token records of
-    # every module (K T 16) + the terminal's gain-gradient partials (ceil(T/32) d 4)
-    # + the terminal's bf16 copy of gain * h (T d 2); no V x d and no T x V piece
-    for K, T, d, V in [(4, 16384, 2048, 32000), (2, 32768, 2048, 128256), (4, 8192, 1024, 32000), (1, 1, 256, 1)]:
-        want = 3 * al(K * T * 4) + al(K * T * 16) + al(-(-T // 32) * d * 4) + al(T * d * 2)
+    # bf16 matrix-core families: rstd, lse, row_loss (3 K T 4) + per-token records of
+    # every module (K T 16) + the terminal's gain-gradient partials (one row of d fp32
+    # per token tile: 64-row tiles at d <= 1024, 32-row tiles up to 2048, 16-row tiles
+    # at d = 2560) + the terminal's bf16 copy of gain * h (T d 2); no V x d and no T x V piece
+    for K, T, d, V, rows in [(4, 16384, 2048, 32000, 32), (2, 32768, 2048, 128256, 32), (4, 8192, 1024, 32000, 64),
+                             (1, 1, 256, 1, 64), (3, 100, 1536, 50, 32), (8, 16384, 2560, 32000, 16)]:
+        want = 3 * al(K * T * 4) + al(K * T * 16) + al(-(-T // rows) * d * 4) + al(T * d * 2)
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, True) == want
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == 3 * al(K * T * 4)
     # the workspace does not depend on V at all
@@ -177,7 +179,7 @@ def test_args_struct_layout_matches_header(tmp_path):
 def test_general_workspace_sizes():
     K, T, d, V = 3, 40, 256, 100
     kt = K * T
-    tiles = -(-T // 32)
+    tiles = -(-T // 64)  # 64-row token tiles of the matrix-core kernels at d <= 1024
     head = B.workspace_size(K, T, d, V, B.SOLO_BF16, True)
     # the headline arguments through the general entry point: same workspace
     assert B.general_workspace_size(gargs()) == head
