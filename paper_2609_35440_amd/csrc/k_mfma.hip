@@ -54,21 +54,27 @@ constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: c
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
 
 // Stationary rows per workgroup: 64 while the accumulator (64 rows x d/8
-// columns) and the stationary operand fit the register file (d <= 1024),
-// 32 otherwise.  The readout streamed per flop halves with the taller tile.
-template <int DS>
-constexpr int rows_of() { return DS <= 128 ? 64 : 32; }
+// columns) and the stationary operand fit the register file (d <= 1024), or
+// in the passes without a second product (no accumulator) up to d = 2048; 32
+// otherwise.  The readout streamed per flop halves with the taller tile.
+template <int DS, bool PC>
+constexpr int rows_of() { return (DS <= 128 || (!PC && DS <= 256)) ? 64 : 32; }
 
-template <int DS>
+template <int DS, bool PC>
 struct Geo : layout::Geo<DS> {
-    static constexpr int XR = rows_of<DS>();           // stationary rows per workgroup
+    static constexpr int XR = rows_of<DS, PC>();       // stationary rows per workgroup
+    // rows of the partial-logit exchange buffer: 64-row tiles at the widest
+    // slices exchange their logits in two rounds of 32 rows (LDS budget)
+    static constexpr int PR = (XR == 64 && DS > 128) ? 32 : XR;
+    static constexpr int NX = XR / PR;                 // exchange rounds per chunk
     static constexpr int NXB = XR / 16;                // 16-row blocks of the logit product
     static constexpr int NR = XR / 32;                 // rows per lane in the elementwise step = 32-row
                                                        // halves of the second product
     static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
     static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
     static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
-    static constexpr int TOTAL = 2 * YBUF + NW * XR * PP * 4 + XR * YC * 2 + 2 * XR * 4 + NW * XR * 4 + 4 * YC * 4;
+    static constexpr int GB = PC ? XR * YC : 8;        // elements of the probability tile (second product only)
+    static constexpr int TOTAL = 2 * YBUF + NW * PR * PP * 4 + GB * 2 + 2 * XR * 4 + NW * XR * 4 + 4 * YC * 4;
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
@@ -81,11 +87,12 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
 // EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
-    using G = Geo<DS>;
+    constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
+    using G = Geo<DS, PC>;
     constexpr int XR = G::XR;
     constexpr int NR = G::NR;
+    constexpr int PR = G::PR;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
-    constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
     // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
     // the logit products, [kDmaA, NI) after the elementwise step (at d = 2048:
@@ -95,8 +102,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
     __shared__ __attribute__((aligned(16))) char ybufB[G::YBUF];
-    __shared__ __attribute__((aligned(16))) float part[NW * XR * PP];
-    __shared__ __attribute__((aligned(16))) bf16 gbuf[XR * YC];
+    __shared__ __attribute__((aligned(16))) float part[NW * PR * PP];
+    __shared__ __attribute__((aligned(16))) bf16 gbuf[G::GB];
     __shared__ float abuf[XR];
     __shared__ float sbuf[XR];
     __shared__ float cbuf[NW * XR];
@@ -255,19 +262,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 __builtin_amdgcn_sched_barrier(0);  // keeps the instruction between these products
             }
         }
+        const int yg = y0 + yy;
+#pragma unroll
+        for (int rr = 0; rr < G::NX; ++rr) {
+        // exchange round rr: the partials of stationary rows [rr PR, (rr + 1) PR)
+        if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
-        for (int xb = 0; xb < G::NXB; ++xb)
-            *(f32x4*)(part + (w * XR + 16 * xb + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
+        for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb)
+            *(f32x4*)(part + (w * PR + 16 * xb - PR * rr + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
         lds_barrier();
 
         // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
-        const int yg = y0 + yy;
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
+        for (int r = rr * (NR / G::NX); r < (rr + 1) * (NR / G::NX); ++r) {
         float q[NW];
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo[r]) * PP + yy];
+        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xo[r] - PR * rr) * PP + yy];
         static_assert(NW == 8, "partial-sum tree");
         const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
         float gval = 0.f;
@@ -306,6 +317,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             db_part[r] += dlt;
         }
         if (PC) gbuf[xo[r] * YC + yy] = (bf16)gval;
+        }
         }
         if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
         lds_barrier();
@@ -531,7 +543,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 template <int MODE, int DS, bool EXT>
 hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
     const bool ll = MODE == LOCAL || MODE == EVAL;
-    constexpr int XR = Geo<DS>::XR;
+    constexpr int XR = Geo<DS, MODE == LOCAL || MODE == RGRAD>::XR;
     dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
                    : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
@@ -557,7 +569,7 @@ hipError_t launch_mode(const FusedArgs& a, int nmod, hipStream_t s) {
 
 bool mfma_supported(int dtype, int d) { return dtype == 0 && d % (NW * 32) == 0 && d >= NW * 32 && d <= NW * 256; }
 
-int mfma_rows(int d) { return d <= NW * 128 ? rows_of<128>() : rows_of<256>(); }
+int mfma_rows(int d) { return d <= NW * 128 ? rows_of<128, true>() : rows_of<256, true>(); }
 
 hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s) {
     return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
