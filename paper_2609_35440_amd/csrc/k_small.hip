@@ -15,14 +15,21 @@ __device__ __forceinline__ float to_f32(float x) { return x; }
 // rstd[row] = 1 / sqrt(mean_j h[row][j]^2 + eps); one wave per row.
 template <typename E>
 __global__ void k_row_rstd(const E* __restrict__ h, float* __restrict__ rstd, long long rows, int d, float eps) {
+    // one wave per row, 16 bytes per lane per load (d % 8 == 0 and 16-byte aligned rows)
+    constexpr int VE = 16 / (int)sizeof(E);
+    typedef E ev __attribute__((ext_vector_type(VE)));
     const int lane = threadIdx.x & 63;
     long long row = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
     if (row >= rows) return;
     const E* x = h + row * (long long)d;
     float acc = 0.f;
-    for (int j = lane; j < d; j += 64) {
-        float v = to_f32(x[j]);
-        acc = fmaf(v, v, acc);
+    for (int j = lane * VE; j < d; j += 64 * VE) {
+        const ev v = *(const ev*)(x + j);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+            const float f = to_f32(v[e]);
+            acc = fmaf(f, f, acc);
+        }
     }
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
     if (lane == 0) {
