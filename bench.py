@@ -132,14 +132,22 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "he
     }
 
 
-def kernel_sources_hash() -> str:
-    """Hash of the matrix-core kernel sources (stamps counter-derived traffic)."""
+def kernel_sources_hash(read=None) -> str:
+    """Hash of the matrix-core kernel sources, comments and whitespace removed
+    (stamps counter-derived traffic: a comment edit does not void a measurement)."""
     import hashlib
+    import re
+
+    if read is None:
+        def read(f):
+            with open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f), "rb") as fh:
+                return fh.read().decode()
 
     h = hashlib.sha256()
     for f in ("k_mfma.hip", "mfma_common.h", "mfma_layout.h", "solo_internal.h"):
-        with open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        text = re.sub(r"/\*.*?\*/", " ", read(f), flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

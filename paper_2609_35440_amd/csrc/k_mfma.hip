@@ -9,7 +9,7 @@
 //   z_tv = tau_k r_t <R_kv, g_k * h_t> + b_kv
 //
 //   local-loss pass (every module; Eq. 2 and Eq. 3):
-//     stationary X = 32 rows t of g_k * h_k, streamed Y = the readout rows v,
+//     stationary X = XR rows t of g_k * h_k, streamed Y = the readout rows v,
 //     online (max, sum-exp) per row, and acc_t += sum_v exp(z_tv - m_t) R_kv,
 //     so that dhhat_t = tau_k (acc_t / s_t - R_{k,y_t}) / T at the end, followed
 //     by the RMSNorm backward and, for a module that trains its gain, the
@@ -20,7 +20,7 @@
 //     row (lowest index on ties) next to its loss.
 //
 //   readout-gradient pass (modules whose readout is trained):
-//     stationary X = 32 readout rows v, streamed Y = the rows t of g_k * h_k
+//     stationary X = XR readout rows v, streamed Y = the rows t of g_k * h_k
 //     (a copy rounded like the local-loss pass's stationary tile, so both
 //     passes multiply the same operands), delta_tv = (exp(z_tv - lse_t) -
 //     [v = y_t]) / T and dR_v = sum_t delta_tv tau_k r_t (g_k * h_t),
@@ -29,15 +29,16 @@
 //   bias-gradient pass: the readout-gradient pass without the second product,
 //     for modules whose bias is trained but whose readout is not.
 //
-// Work split: a workgroup of 8 waves owns the 32 stationary rows; wave w owns
-// the d/8 columns [w d/8, (w+1) d/8).  Per chunk of 16 streamed rows, every
-// wave multiplies its column slice (split-K partial of the logit tile), the
-// partials meet in LDS, each wave finishes the elementwise step for 4 of the
-// 32 stationary rows, and every wave then accumulates its own column slice of
-// the second product.  The accumulator (32 rows x d/8 columns, fp32) and the
-// stationary operand stay in registers for the whole pass; the streamed
-// chunk goes HBM/L2 -> LDS directly and is read twice from LDS: row-wise for
-// the logit product and with the transposing read for the second product.
+// Work split: a workgroup of 8 waves owns XR stationary rows (32, or 64 where
+// the register file allows it: see rows_of); wave w owns the d/8 columns
+// [w d/8, (w+1) d/8).  Per chunk of 16 streamed rows, every wave multiplies
+// its column slice (split-K partial of the logit tile), the partials meet in
+// LDS, each wave finishes the elementwise step for XR/8 of the stationary
+// rows, and every wave then accumulates its own column slice of the second
+// product.  The accumulator (XR rows x d/8 columns, fp32) and the stationary
+// operand stay in registers for the whole pass; the streamed chunk goes
+// HBM/L2 -> LDS directly and is read twice from LDS: row-wise for the logit
+// product and with the transposing read for the second product.
 #include "mfma_common.h"
 
 namespace solo {
