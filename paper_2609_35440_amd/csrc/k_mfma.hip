@@ -266,59 +266,59 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         const int yg = y0 + yy;
 #pragma unroll
         for (int rr = 0; rr < G::NX; ++rr) {
-        // exchange round rr: the partials of stationary rows [rr PR, (rr + 1) PR)
-        if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
-        // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
+            // exchange round rr: the partials of stationary rows [rr PR, (rr + 1) PR)
+            if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
+            // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
-        for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb)
-            *(f32x4*)(part + (w * PR + 16 * xb - PR * rr + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
-        lds_barrier();
+            for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb)
+                *(f32x4*)(part + (w * PR + 16 * xb - PR * rr + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
+            lds_barrier();
 
-        // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
+            // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
 #pragma unroll
-        for (int r = rr * (NR / G::NX); r < (rr + 1) * (NR / G::NX); ++r) {
-        float q[NW];
+            for (int r = rr * (NR / G::NX); r < (rr + 1) * (NR / G::NX); ++r) {
+                float q[NW];
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xo[r] - PR * rr) * PP + yy];
-        static_assert(NW == 8, "partial-sum tree");
-        const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
-        float gval = 0.f;
-        if (LL) {
-            // columns past the end of the vocabulary get z = -inf (an additive
-            // mask rather than a branch, so the partial reads stay unconditional)
-            float ymask = (yg < nY) ? 0.f : -INFINITY;
-            if (BZ && has_bias) ymask += side[yy] * kLog2e;
-            const float zc = __builtin_fmaf(sxy, own_r2[r], ymask);
-            float alpha = 1.f;
-            if (__builtin_expect(__any(zc > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
-                const float cmax = row16_max(zc);
-                if (cmax > m_run[r] + kLazyThresh2) {
-                    alpha = __builtin_amdgcn_exp2f(m_run[r] - cmax);
-                    s_part[r] *= alpha;
-                    m_run[r] = cmax;
+                for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xo[r] - PR * rr) * PP + yy];
+                static_assert(NW == 8, "partial-sum tree");
+                const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
+                float gval = 0.f;
+                if (LL) {
+                    // columns past the end of the vocabulary get z = -inf (an additive
+                    // mask rather than a branch, so the partial reads stay unconditional)
+                    float ymask = (yg < nY) ? 0.f : -INFINITY;
+                    if (BZ && has_bias) ymask += side[yy] * kLog2e;
+                    const float zc = __builtin_fmaf(sxy, own_r2[r], ymask);
+                    float alpha = 1.f;
+                    if (__builtin_expect(__any(zc > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
+                        const float cmax = row16_max(zc);
+                        if (cmax > m_run[r] + kLazyThresh2) {
+                            alpha = __builtin_amdgcn_exp2f(m_run[r] - cmax);
+                            s_part[r] *= alpha;
+                            m_run[r] = cmax;
+                        }
+                    }
+                    const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
+                    s_part[r] += p;
+                    if (yg == own_tgt[r]) zy_part[r] = zc;
+                    if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
+                        best[r] = zc;
+                        best_v[r] = yg;
+                    }
+                    gval = p;
+                    if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
+                } else {
+                    // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
+                    // the end of the module read as zeros and are masked
+                    const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
+                    // (a padded token's zero record would match readout row 0 as its target)
+                    const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
+                    gval = dlt * r4[3];
+                    db_part[r] += dlt;
                 }
+                if (PC) gbuf[xo[r] * YC + yy] = (bf16)gval;
             }
-            const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
-            s_part[r] += p;
-            if (yg == own_tgt[r]) zy_part[r] = zc;
-            if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
-                best[r] = zc;
-                best_v[r] = yg;
-            }
-            gval = p;
-            if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
-        } else {
-            // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
-            // the end of the module read as zeros and are masked
-            const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
-            // (a padded token's zero record would match readout row 0 as its target)
-            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
-            gval = dlt * r4[3];
-            db_part[r] += dlt;
-        }
-        if (PC) gbuf[xo[r] * YC + yy] = (bf16)gval;
-        }
         }
         if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
         lds_barrier();
