@@ -27,7 +27,11 @@ struct Geo {
     static constexpr bool PADDED = (NI % 4) == 0 && (512 % DS) == 0;
     static constexpr int IPITCH = PADDED ? 1088 : 1024;     // bytes between the instructions' destinations
     static constexpr int SLICE = (NI - 1) * IPITCH + 1024;  // bytes of one wave's chunk slice
-    static constexpr int NV = PADDED ? NI / 2 : NI;         // distinct per-lane stream offsets
+    // XOR key of the padded layout: (r >> KS) & 3 (see phys); chosen per width
+    // by measurement: KS = 1 (both reads conflict-free under the bank model)
+    // is 2% faster at DS = 256, KS = 2 is 1.5% faster at DS = 128
+    static constexpr int KS = DS >= 256 ? 1 : 2;
+    static constexpr int NV = PADDED ? (NI >> KS) : NI;     // distinct per-lane stream offsets
     static_assert(DS % 32 == 0 && DS >= 32 && DS <= 512, "slice width");
 };
 
@@ -37,20 +41,21 @@ struct Geo {
 // Padded layout: instruction q of the direct-to-LDS stream writes rows
 // q, q + NI, ... (one row if DS = 512) back to back at q * 1088 (so its rows
 // start at byte 64 q mod 256); inside a row, the low two bits of the granule
-// index are XORed with (r >> 1) & 3.  Under the LDS service model measured on
+// index are XORed with (r >> KS) & 3.  Under the LDS service model measured on
 // gfx950 (a 16-byte-per-lane read served 8 lanes over 32 banks per pass, the
-// 8-byte transposing read 32 lanes over 64 banks) both read patterns are then
-// conflict-free: the row-wise reads (16 rows at one granule: rows r and r + 1
-// differ in the start bank of their instruction, pairs of rows in the XOR key)
-// and the transposing reads (4 rows x 4 granules).  The offset stays additive
-// in g >> 2, so unrolled loops address with immediates.
+// 8-byte transposing read 32 lanes over 64 banks) the transposing reads (4
+// rows x 4 granules) are conflict-free with either key; with KS = 1 the
+// row-wise reads (16 rows at one granule) are too (rows r and r + 1 differ in
+// the start bank of their instruction, pairs of rows in the XOR key), with
+// KS = 2 they are 2-way.  The offset stays additive in g >> 2, so unrolled
+// loops address with immediates.
 // Linear layout (other widths): rows back to back.
 template <int DS>
 SOLO_HD int phys(int r, int g) {
     using G = Geo<DS>;
     if constexpr (G::PADDED) {
         const int q = r % G::NI, k = r / G::NI;
-        return q * G::IPITCH + k * (DS * 2) + 16 * (4 * (g >> 2) + ((g & 3) ^ ((r >> 1) & 3)));
+        return q * G::IPITCH + k * (DS * 2) + 16 * (4 * (g >> 2) + ((g & 3) ^ ((r >> G::KS) & 3)));
     } else {
         return (r * G::GPR + g) * 16;
     }
@@ -72,19 +77,19 @@ SOLO_HD int stream_row0(int q) {
 // Which per-lane offset register instruction q uses.
 template <int DS>
 SOLO_HD int stream_vidx(int q) {
-    return Geo<DS>::PADDED ? (q >> 1) : q;
+    return Geo<DS>::PADDED ? (q >> Geo<DS>::KS) : q;
 }
 
 // Per-lane byte offset for offset register v (0 .. NV-1), width d, slice start js.
 // Padded: instruction q fetches rows q + NI k (k = lane / GPR); the offset
-// depends on q only through q >> 1 (NI is even, so (r >> 1) & 3 of row
-// q + NI k is ((q >> 1) + (NI / 2) k) & 3).
+// depends on q only through q >> KS (NI is a multiple of 4, so (r >> KS) & 3
+// of row q + NI k is ((q >> KS) + (NI >> KS) k) & 3).
 template <int DS>
 SOLO_HD int stream_voff(int v, int d, int js, int lane) {
     using G = Geo<DS>;
     if constexpr (G::PADDED) {
         const int k = lane / G::GPR, s = lane % G::GPR;
-        const int x = (v + (G::NI / 2) * k) & 3;  // (r >> 1) & 3 of row r = q + NI k with q >> 1 = v
+        const int x = (v + (G::NI >> G::KS) * k) & 3;  // (r >> KS) & 3 of row r = q + NI k with q >> KS = v
         const int g = 4 * (s >> 2) + ((s & 3) ^ x);
         return (G::NI * k * d + js + 8 * g) * 2;
     } else {
