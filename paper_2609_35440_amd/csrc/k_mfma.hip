@@ -456,7 +456,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (ehh == 0) cbuf[w * XR + 32 * h + ex] = cp;
         }
         __syncthreads();
-        // sweep 2: dh = r (dn - c n)
+        // sweep 2: dh = r (dn - c n).  The accumulator layout gives a lane 8
+        // bytes of a row per store (16 contiguous bytes per row and
+        // instruction), which the memory system writes back as partial lines.
+        // The 32 rows of a half-tile are staged in this wave's two (now idle)
+        // chunk slices instead, 16 rows each, granule g of row r at g ^ (r & SM),
+        // and leave as whole row segments of the wave's columns.
+        constexpr int GS = DS / 8;  // 16-byte granules per row of the wave's columns
+        constexpr int SM = (GS % 16 == 0) ? 15 : ((GS % 8 == 0) ? 7 : 3);
+        static_assert(GS % 4 == 0 && 16 * 2 * DS <= G::SLICE, "staging rows fit a chunk slice");
 #pragma unroll
         for (int h = 0; h < NR; ++h) {
             const int xg = x0 + 32 * h + ex;
@@ -465,25 +473,32 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + 32 * h + ex];
             const float cmean = tau_k * csum / (float)d;
             if (a.rowdtau && w == 0 && ehh == 0 && xok[h]) a.rowdtau[modoff + xg] = tok[h] ? csum : 0.f;
-            if (xok[h]) {
-                bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
+            LDS_AS char* srow = (ex < 16 ? sliceA : sliceB) + (ex & 15) * (2 * DS);
 #pragma unroll
-                for (int b = 0; b < (PC ? G::NB : 1); ++b) {
+            for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
-                    for (int i4 = 0; i4 < 4; ++i4) {
-                        const int j = js + 32 * b + 8 * i4 + 4 * ehh;
-                        const u16x4 hv = *(const u16x4*)(hrow[h] + j);
-                        const u16x4 gv = *(const u16x4*)(gk + j);
-                        bf16x4 o;
+                for (int i4 = 0; i4 < 4; ++i4) {
+                    const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                    const u16x4 hv = *(const u16x4*)(hrow[h] + j);  // row 0 for rows past the end
+                    const u16x4 gv = *(const u16x4*)(gk + j);
+                    bf16x4 o;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float n = rx[h] * bf16_bits_to_f32(hv[e]);
-                            o[e] = (bf16)(rx[h] * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][h][4 * i4 + e] - cmean * n));
-                        }
-                        *(bf16x4*)(dhrow + j) = o;
+                    for (int e = 0; e < 4; ++e) {
+                        const float n = rx[h] * bf16_bits_to_f32(hv[e]);
+                        o[e] = (bf16)(rx[h] * (tau_k * bf16_bits_to_f32(gv[e]) * acc[b][h][4 * i4 + e] - cmean * n));
                     }
-                    __builtin_amdgcn_sched_barrier(0);
+                    *(LDS_AS bf16x4*)(srow + 16 * ((4 * b + i4) ^ (ex & SM)) + 8 * ehh) = o;
                 }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            // lane p of store q moves granule slot 64 q + p of the 32 x GS staged granules
+#pragma unroll
+            for (int q = 0; q < GS / 2; ++q) {
+                const int sl = 64 * q + lane, row = sl / GS, g = sl % GS;
+                const i32x4 v = *(LDS_AS i32x4*)((row < 16 ? sliceA : sliceB) + (row & 15) * (2 * DS) +
+                                                 16 * (g ^ (row & SM)));
+                const int xr = x0 + 32 * h + row;
+                if (xr < nX) *(i32x4*)((bf16*)a.dh + (modoff + xr) * (long long)d + js + 8 * g) = v;
             }
         }
         // sweep 3, for a module that trains its gain: the tile's partial sums
