@@ -32,6 +32,9 @@ CASES = [
     ("wide_d2560_V1", "2b", dict(K=2, T=20, d=2560, V=1), True),
     ("wide_d2560_T1", "2b", dict(K=2, T=1, d=2560, V=77), True),
     ("valu_d72", "340m", dict(K=2, T=10, d=72, V=50), True),
+    ("valu_d3072", "2b", dict(K=2, T=9, d=3072, V=37), True),
+    ("valu_d4096_max", "1b", dict(K=2, T=5, d=4096, V=33), True),
+    ("f32_d4096_max", "tiny", dict(K=2, T=4, d=4096, V=19), True),
     ("mfma_V1", "340m", dict(K=2, T=40, d=256, V=1), True),
     ("mfma_V2", "340m", dict(K=2, T=40, d=256, V=2), True),
     ("mfma_T1", "340m", dict(K=2, T=1, d=256, V=60), True),
