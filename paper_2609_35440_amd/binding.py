@@ -187,6 +187,76 @@ def _dtype_code(t):
     raise TypeError(f"unsupported dtype {t}; use torch.bfloat16 or torch.float32")
 
 
+def _check_targets(targets):
+    import torch
+
+    if targets.dtype.is_floating_point or targets.dtype.is_complex or targets.dtype == torch.bool:
+        raise TypeError(f"targets must be an integer tensor, got {targets.dtype}")
+
+
+def _check_device(dev, tensors):
+    for name, t in tensors.items():
+        if t is not None and t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, expected {dev} (all tensors on one GPU)")
+
+
+def _check_out(out, spec, dev):
+    """Every output this call writes must match (shape, dtype), sit on ``dev`` and be
+    contiguous: the kernels write its full extent through its data pointer.  Returns
+    name -> tensor for the outputs written, None for the others (whose pointers stay NULL)."""
+    used = {}
+    for name, (shape, dtype) in spec.items():
+        t = getattr(out, name)
+        used[name] = None
+        if shape is None:
+            continue
+        if t is None:
+            raise ValueError(f"out.{name} is required for this call")
+        if tuple(t.shape) != tuple(shape) or t.dtype != dtype or t.device != dev or not t.is_contiguous():
+            raise ValueError(f"out.{name}: expected contiguous {dtype} {tuple(shape)} on {dev}, "
+                             f"got {'contiguous' if t.is_contiguous() else 'non-contiguous'} {t.dtype} "
+                             f"{tuple(t.shape)} on {t.device}")
+        used[name] = t
+    return used
+
+
+def _workspace(workspace, ws_bytes, dev):
+    import torch
+
+    if workspace is not None:
+        if workspace.device != dev or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the inputs' GPU")
+        if workspace.numel() * workspace.element_size() >= ws_bytes:
+            return workspace
+    return torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
+
+def _streams(stream, dev):
+    """The stream the call is enqueued on, and torch's current stream, on which the
+    input conversions and new tensors of this call were made.  A different call
+    stream first waits for the current one."""
+    import torch
+
+    cur = torch.cuda.current_stream(dev)
+    if stream is None:
+        return cur, cur
+    if stream.device != dev:
+        raise ValueError(f"stream is on {stream.device}, expected {dev}")
+    if stream != cur:
+        stream.wait_stream(cur)
+    return stream, cur
+
+
+def _hand_over(stream, cur, tensors):
+    """Tensors made on ``cur`` and used on another ``stream``: tell the caching
+    allocator, so that their memory is not reused before the stream has finished."""
+    if stream == cur:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 def readout_fwd_bwd(h, gain, W, targets, final_module_dW: bool = True, eps: float = 1e-6, *,
                     row_loss: bool = False, workspace=None, out: Optional[ReadoutResult] = None,
                     stream=None, stage_events=None) -> ReadoutResult:
@@ -210,35 +280,41 @@ def readout_fwd_bwd(h, gain, W, targets, final_module_dW: bool = True, eps: floa
         raise TypeError("h, gain and W must share one dtype")
     if not (h.is_cuda and gain.is_cuda and W.is_cuda and targets.is_cuda):
         raise ValueError("all inputs must be GPU tensors")
+    _check_targets(targets)
     dt = _dtype_code(h.dtype)
     dev = h.device
+    _check_device(dev, {"gain": gain, "W": W, "targets": targets})
     h = h.contiguous()
     gain = gain.contiguous()
     W = W.contiguous()
-    if targets.dtype != torch.int32:
-        targets = targets.to(torch.int32)
-    targets = targets.contiguous()
+    targets = targets.to(torch.int32).contiguous()
 
     fdw = bool(final_module_dW)
+    f32 = torch.float32
+    made = []
     if out is None:
         out = ReadoutResult(
-            losses=torch.empty(K, dtype=torch.float32, device=dev),
+            losses=torch.empty(K, dtype=f32, device=dev),
             dh=torch.empty_like(h),
-            dW=torch.empty((V, d), dtype=torch.float32, device=dev) if fdw else None,
-            dgain=torch.empty(d, dtype=torch.float32, device=dev) if fdw else None,
-            row_loss=torch.empty((K, T), dtype=torch.float32, device=dev) if row_loss else None,
+            dW=torch.empty((V, d), dtype=f32, device=dev) if fdw else None,
+            dgain=torch.empty(d, dtype=f32, device=dev) if fdw else None,
+            row_loss=torch.empty((K, T), dtype=f32, device=dev) if row_loss else None,
         )
+        made = list(out)
+    none = (None, None)
+    used = _check_out(out, {"losses": ((K,), f32), "dh": ((K, T, d), h.dtype),
+                            "dW": ((V, d), f32) if fdw else none, "dgain": ((d,), f32) if fdw else none,
+                            "row_loss": ((K, T), f32) if out.row_loss is not None else none}, dev)
     ws_bytes = workspace_size(K, T, d, V, dt, fdw)
     if ws_bytes == 0:
         raise SoloError(STATUS["SOLO_ERR_SHAPE"], status_string(STATUS["SOLO_ERR_SHAPE"]))
-    if workspace is None or workspace.numel() * workspace.element_size() < ws_bytes:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    if stream is None:
-        stream = torch.cuda.current_stream(dev)
+    workspace = _workspace(workspace, ws_bytes, dev)
+    stream, cur = _streams(stream, dev)
+    _hand_over(stream, cur, [h, gain, W, targets, workspace] + made)
     st = readout_fwd_bwd_raw(
         K, T, d, V, dt, eps, h.data_ptr(), gain.data_ptr(), W.data_ptr(), targets.data_ptr(), fdw,
-        out.losses.data_ptr(), out.row_loss.data_ptr() if out.row_loss is not None else 0, out.dh.data_ptr(),
-        out.dW.data_ptr() if fdw else 0, out.dgain.data_ptr() if fdw else 0,
+        used["losses"].data_ptr(), _ptr(used["row_loss"]) or 0, used["dh"].data_ptr(),
+        _ptr(used["dW"]) or 0, _ptr(used["dgain"]) or 0,
         workspace.data_ptr(), workspace.numel() * workspace.element_size(), stream.cuda_stream, stage_events)
     if st != 0:
         raise SoloError(st, status_string(st))
@@ -290,6 +366,8 @@ def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps):
     for t in (h, gain, W, targets, Wbar, tau, bias):
         if t is not None and not t.is_cuda:
             raise ValueError("all inputs must be GPU tensors")
+    _check_targets(targets)
+    _check_device(h.device, {"gain": gain, "W": W, "targets": targets, "Wbar": Wbar, "tau": tau, "bias": bias})
     keep = {
         "h": h.contiguous(), "gain": gain.contiguous(), "W": W.contiguous(),
         "Wbar": Wbar.contiguous() if Wbar is not None else None,
@@ -326,29 +404,41 @@ def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, fina
     f32 = dict(dtype=torch.float32, device=dev)
     fdw = bool(final_module_dW)
     priv = bool(heads_train_readout)
-    out = out if out is not None else GeneralResult(
-        losses=torch.empty(K, **f32),
-        dh=torch.empty_like(keep["h"]),
-        dW=torch.empty((V, d), **f32) if fdw else None,
-        dWbar=torch.empty((K - 1, V, d), **f32) if (priv and K > 1) else None,
-        dgain=(torch.empty((K, d), **f32) if a.gain_per_module else (torch.empty(d, **f32) if fdw else None)),
-        dtau=torch.empty(K, **f32) if want_dtau else None,
-        dbias=torch.empty((K, V), **f32) if want_dbias else None,
-        row_loss=torch.empty((K, T), **f32) if row_loss else None,
-    )
+    made = []
+    if out is None:
+        out = GeneralResult(
+            losses=torch.empty(K, **f32),
+            dh=torch.empty_like(keep["h"]),
+            dW=torch.empty((V, d), **f32) if fdw else None,
+            dWbar=torch.empty((K - 1, V, d), **f32) if (priv and K > 1) else None,
+            dgain=(torch.empty((K, d), **f32) if a.gain_per_module else (torch.empty(d, **f32) if fdw else None)),
+            dtau=torch.empty(K, **f32) if want_dtau else None,
+            dbias=torch.empty((K, V), **f32) if want_dbias else None,
+            row_loss=torch.empty((K, T), **f32) if row_loss else None,
+        )
+        made = list(out)
+    fl = torch.float32
+    none = (None, None)
+    used = _check_out(out, {
+        "losses": ((K,), fl), "dh": ((K, T, d), keep["h"].dtype),
+        "dW": ((V, d), fl) if fdw else none,
+        "dWbar": ((K - 1, V, d), fl) if (priv and K > 1) else none,
+        "dgain": ((K, d), fl) if a.gain_per_module else (((d,), fl) if fdw else none),
+        "dtau": ((K,), fl) if want_dtau else none,
+        "dbias": ((K, V), fl) if want_dbias else none,
+        "row_loss": ((K, T), fl) if out.row_loss is not None else none}, dev)
     a.final_module_dW = int(fdw)
     a.heads_train_readout = int(priv)
     for name in ("losses", "dh", "dW", "dWbar", "dgain", "dtau", "dbias", "row_loss"):
-        setattr(a, name, _ptr(getattr(out, name)))
+        setattr(a, name, _ptr(used[name]))
     ws_bytes = general_workspace_size(a)
     if ws_bytes == 0:
         raise SoloError(STATUS["SOLO_ERR_SHAPE"], status_string(STATUS["SOLO_ERR_SHAPE"]))
-    if workspace is None or workspace.numel() * workspace.element_size() < ws_bytes:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, ws_bytes, dev)
     a.workspace = workspace.data_ptr()
     a.workspace_bytes = workspace.numel() * workspace.element_size()
-    if stream is None:
-        stream = torch.cuda.current_stream(dev)
+    stream, cur = _streams(stream, dev)
+    _hand_over(stream, cur, list(keep.values()) + [workspace] + made)
     a.hip_stream = stream.cuda_stream or None
     evs = None
     if stage_events is not None:
@@ -370,23 +460,28 @@ def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float
     a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
     K, T = a.K, a.T
     dev = h.device
-    out = out if out is not None else EvalResult(
-        losses=torch.empty(K, dtype=torch.float32, device=dev),
-        row_loss=torch.empty((K, T), dtype=torch.float32, device=dev) if row_loss else None,
-        top1=torch.empty((K, T), dtype=torch.int32, device=dev) if top1 else None,
-    )
-    a.losses = _ptr(out.losses)
-    a.row_loss = _ptr(out.row_loss)
-    a.top1 = _ptr(out.top1)
+    made = []
+    if out is None:
+        out = EvalResult(
+            losses=torch.empty(K, dtype=torch.float32, device=dev),
+            row_loss=torch.empty((K, T), dtype=torch.float32, device=dev) if row_loss else None,
+            top1=torch.empty((K, T), dtype=torch.int32, device=dev) if top1 else None,
+        )
+        made = list(out)
+    used = _check_out(out, {"losses": ((K,), torch.float32),
+                            "row_loss": ((K, T), torch.float32) if out.row_loss is not None else (None, None),
+                            "top1": ((K, T), torch.int32) if out.top1 is not None else (None, None)}, dev)
+    a.losses = _ptr(used["losses"])
+    a.row_loss = _ptr(used["row_loss"])
+    a.top1 = _ptr(used["top1"])
     ws_bytes = exit_eval_workspace_size(a)
     if ws_bytes == 0:
         raise SoloError(STATUS["SOLO_ERR_SHAPE"], status_string(STATUS["SOLO_ERR_SHAPE"]))
-    if workspace is None or workspace.numel() * workspace.element_size() < ws_bytes:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    workspace = _workspace(workspace, ws_bytes, dev)
     a.workspace = workspace.data_ptr()
     a.workspace_bytes = workspace.numel() * workspace.element_size()
-    if stream is None:
-        stream = torch.cuda.current_stream(dev)
+    stream, cur = _streams(stream, dev)
+    _hand_over(stream, cur, list(keep.values()) + [workspace] + made)
     a.hip_stream = stream.cuda_stream or None
     evs = None
     if stage_events is not None:
