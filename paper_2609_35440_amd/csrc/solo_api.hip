@@ -149,7 +149,6 @@ int run(const solo_readout_args& x, bool eval) {
     const int K = x.K, T = x.T, d = x.d, V = x.V;
     hipStream_t s = (hipStream_t)x.hip_stream;
     char* ws = (char*)x.workspace;
-    const size_t elem = x.dtype == SOLO_BF16 ? 2 : 4;
 
     solo::FusedArgs a = {};
     a.K = K;
@@ -182,7 +181,6 @@ int run(const solo_readout_args& x, bool eval) {
     a.dWt = (!eval && x.final_module_dW) ? x.dW : nullptr;
     a.dWh = (!eval && x.heads_train_readout) ? x.dWbar : nullptr;
     a.dbias = eval ? nullptr : x.dbias;
-    (void)elem;
 
     auto mark = [&](int stage) -> bool {
         if (!x.stage_events || !x.stage_events[stage]) return true;
