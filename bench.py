@@ -84,6 +84,17 @@ class EventSet:
             self.hip.hipEventDestroy(ctypes.c_void_p(e))
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "headline") -> dict:
     """fp64 oracle on the same workload restricted to sample_T tokens per module."""
     import numpy as np
@@ -120,10 +131,18 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "he
                                    heads_train_readout=flags.get("heads_train_readout", False), **kw)
     dt = time.perf_counter() - t0
     cfg = x["cfg"]
+    from paper_2609_35440_amd import costmodel
+
+    fl = dict(final_module_dW=True) if flags is None else flags
+    alg = costmodel.general_flops(cfg.K, sample_T, cfg.V, cfg.d, final_module_dW=fl.get("final_module_dW", True),
+                                  heads_train_readout=fl.get("heads_train_readout", False),
+                                  exit_eval=extras is not None and flags is None)
     return {
         "value": sample_T / dt,
         "unit": "tokens/s",
         "cores": int(threads),
+        "cpu_model": _cpu_model(),
+        "gflops_algorithmic": alg / dt / 1e9,
         "kind": "oracle",
         "sample": f"{cfg_name} shape with T={sample_T} tokens per module (K={cfg.K}, d={cfg.d}, V={cfg.V}, "
                   f"{'final-module dW included' if variant == 'headline' else 'variant ' + variant}), "
