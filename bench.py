@@ -207,8 +207,8 @@ def main(argv=None) -> int:
         return copy_probe(args.copy_probe)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md, 'How the path would "
-              "shard'); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (no collectives, no sharding); "
+              "run with --gpus 1", file=sys.stderr)
         return 2
 
     import numpy as np
