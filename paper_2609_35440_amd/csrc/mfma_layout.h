@@ -27,10 +27,10 @@ struct Geo {
     static constexpr bool PADDED = (NI % 4) == 0 && (512 % DS) == 0;
     static constexpr int IPITCH = PADDED ? 1088 : 1024;     // bytes between the instructions' destinations
     static constexpr int SLICE = (NI - 1) * IPITCH + 1024;  // bytes of one wave's chunk slice
-    // XOR key of the padded layout: (r >> KS) & 3 (see phys); chosen per width
-    // by measurement: KS = 1 (both reads conflict-free under the bank model)
-    // is 2% faster at DS = 256, KS = 2 is 1.5% faster at DS = 128
-    static constexpr int KS = DS >= 256 ? 1 : 2;
+    // XOR key of the padded layout: (r >> KS) & 3 (see phys).  KS = 1 makes
+    // both reads conflict-free under the bank model; measured 2% faster than
+    // KS = 2 at DS = 256 and 3% faster at DS = 128
+    static constexpr int KS = 1;
     static constexpr int NV = PADDED ? (NI >> KS) : NI;     // distinct per-lane stream offsets
     static_assert(DS % 32 == 0 && DS >= 32 && DS <= 512, "slice width");
 };
@@ -44,11 +44,11 @@ struct Geo {
 // index are XORed with (r >> KS) & 3.  Under the LDS service model measured on
 // gfx950 (a 16-byte-per-lane read served 8 lanes over 32 banks per pass, the
 // 8-byte transposing read 32 lanes over 64 banks) the transposing reads (4
-// rows x 4 granules) are conflict-free with either key; with KS = 1 the
+// rows x 4 granules) are conflict-free with KS = 1 or 2; with KS = 1 the
 // row-wise reads (16 rows at one granule) are too (rows r and r + 1 differ in
 // the start bank of their instruction, pairs of rows in the XOR key), with
-// KS = 2 they are 2-way.  The offset stays additive in g >> 2, so unrolled
-// loops address with immediates.
+// KS = 2 they would be 2-way.  The offset stays additive in g >> 2, so
+// unrolled loops address with immediates.
 // Linear layout (other widths): rows back to back.
 template <int DS>
 SOLO_HD int phys(int r, int g) {

@@ -26,10 +26,9 @@ def test_layout_reads_match_stream(tmp_path):
                             (384, 4), (512, 4)]
     for key, m in rows.items():
         assert int(m.group(4)) == 0, key
-        if m.group(3) == "1":  # padded layouts (DS = 128, 256, 512): transposing reads conflict-free
+        if m.group(3) == "1":  # padded layouts (DS = 128, 256, 512): both read patterns conflict-free
             assert int(m.group(6)) == 0, key
-            if key[0] >= 256:  # ... and, with the key of the wider slices, the row-wise reads too
-                assert int(m.group(5)) == 0, key
+            assert int(m.group(5)) == 0, key
     # the wide layout: every staged write lands once and every read returns its operand;
     # at the shipped width (320 columns per wave) all three access patterns are conflict-free
     wide = {int(m.group(1)): m for m in re.finditer(
