@@ -50,7 +50,13 @@ using namespace mfma;
 constexpr int NW = layout::NW;  // waves per workgroup
 constexpr int NTHR = NW * 64;
 constexpr int YC = layout::YC;  // streamed rows per chunk
-constexpr int PP = 20;       // row pitch (floats) of the partial logit tiles: conflict-free 16 B writes
+// Partial logit tiles part[w][x][y]: rows of PP = 16 floats, the 16-byte
+// group y / 4 of row x stored at (y / 4) ^ ((x >> 1) & 3), so that the 16-byte
+// writes (8 rows at one group per pass) and the elementwise step's reads (4
+// whole rows per wave) are both free of bank conflicts.  The probability tile
+// gbuf[x][y] (bf16, rows of YC) keeps the 16-byte half y / 8 of row x at
+// (y / 8) ^ ((x >> 2) & 1), for its 16-byte reads of 8 rows per pass.
+constexpr int PP = 16;
 
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
 
@@ -270,16 +276,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
             // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
-            for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb)
-                *(f32x4*)(part + (w * PR + 16 * xb - PR * rr + (lane & 15)) * PP + 4 * (lane >> 4)) = S[xb];
+            for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb) {
+                const int xl = 16 * xb - PR * rr + (lane & 15);
+                *(f32x4*)(part + (w * PR + xl) * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) = S[xb];
+            }
             lds_barrier();
 
             // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
 #pragma unroll
             for (int r = rr * (NR / G::NX); r < (rr + 1) * (NR / G::NX); ++r) {
                 float q[NW];
+                const int xl = xo[r] - PR * rr;
+                const int yq = yy ^ (4 * ((xl >> 1) & 3));
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xo[r] - PR * rr) * PP + yy];
+                for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xl) * PP + yq];
                 static_assert(NW == 8, "partial-sum tree");
                 const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
                 float gval = 0.f;
@@ -317,7 +327,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     gval = dlt * r4[3];
                     db_part[r] += dlt;
                 }
-                if (PC) gbuf[xo[r] * YC + yy] = (bf16)gval;
+                if (PC) gbuf[xo[r] * YC + (yy ^ (8 * ((xo[r] >> 2) & 1)))] = (bf16)gval;
             }
         }
         if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
@@ -327,7 +337,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             // ---- second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
             bf16x8 gfrag[NR];
 #pragma unroll
-            for (int h = 0; h < NR; ++h) gfrag[h] = *(bf16x8*)(gbuf + (32 * h + (lane & 31)) * YC + 8 * (lane >> 5));
+            for (int h = 0; h < NR; ++h) {
+                const int xg = 32 * h + (lane & 31);
+                gfrag[h] = *(bf16x8*)(gbuf + xg * YC + 8 * ((lane >> 5) ^ ((xg >> 2) & 1)));
+            }
             if (MODE == LOCAL) {
 #pragma unroll
                 for (int h = 0; h < NR; ++h) {
