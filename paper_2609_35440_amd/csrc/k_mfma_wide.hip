@@ -36,7 +36,12 @@ constexpr int NW = layoutw::NW;  // waves per workgroup
 constexpr int NTHR = NW * 64;
 constexpr int XR = kMfmaWideRows;  // stationary rows per workgroup (16)
 constexpr int YC = layoutw::YC;    // streamed rows per chunk
-constexpr int PP = 20;             // row pitch (floats) of the partial logit tiles
+// Partial logit tiles part[w][x][y]: rows of PP = 16 floats, the 16-byte
+// group y / 4 of row x stored at (y / 4) ^ ((x >> 1) & 3): conflict-free
+// 16-byte writes and row reads.  The probability tile gbuf[x][y] (bf16, rows
+// of YC) keeps the 8-byte group y / 4 of row x at (y / 4) ^ (2 ((x >> 3) & 1)),
+// so that the 8-byte reads of its 16 rows spread over all 64 banks.
+constexpr int PP = 16;
 
 static_assert(XR == 16, "one 16-row block of stationary rows");
 
@@ -215,13 +220,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
             S0 = mfma16(wa, xr[kk], S0);
         }
         // C layout: lane holds S[y = 4 (lane/16) + i][x = lane%16]; store as part[w][x][y]
-        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * (lane >> 4)) = S0;
+        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * ((lane >> 4) ^ (((lane & 15) >> 1) & 3))) = S0;
         lds_barrier();
 
         // ---- (2) elementwise step for rows xo = 2w, 2w+1 (lane: row xo, column yy)
         float q[NW];
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + yy];
+        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + (yy ^ (4 * ((xo >> 1) & 3)))];
         static_assert(NW == 8, "partial-sum tree");
         const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
         const int yg = y0 + yy;
@@ -259,13 +264,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
             gval = dlt * r4[3];
             db_part += dlt;
         }
-        if (PC && wr) gbuf[xo * YC + yy] = (bf16)gval;
+        if (PC && wr) gbuf[xo * YC + (yy ^ (8 * ((xo >> 3) & 1)))] = (bf16)gval;
         lds_barrier();
 
         if (PC) {
             // ---- (3) second product: acc[j][x] += sum_y Y[y][j] G[x][y] over this wave's columns
             // B operand: lane holds G[x = lane%16][y = 4 (lane/16) .. +3]
-            const bf16x4w gfrag = *(LDS_AS bf16x4w*)(gbuf + (lane & 15) * YC + 4 * (lane >> 4));
+            const bf16x4w gfrag =
+                *(LDS_AS bf16x4w*)(gbuf + (lane & 15) * YC + 4 * ((lane >> 4) ^ (2 * ((lane >> 3) & 1))));
             if (MODE == LOCAL) {
                 const float al = abuf[lane & 15];
                 if (__any(al != 1.f)) {
