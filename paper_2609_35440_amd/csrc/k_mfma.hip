@@ -102,9 +102,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
     // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
-    // the logit products, [kDmaA, NI) after the elementwise step (at d = 2048:
-    // 5 and 3 of 8; measured best of 3..8 inside the products)
-    constexpr int kDmaA = (5 * G::NI + 7) / 8;
+    // the logit products, [kDmaA, NI) after the elementwise step.  Measured:
+    // at d = 2048, 5 of 8 inside the products (3 and 8 are 3-5% slower, 4 and 6
+    // within box-to-box noise); at d = 1024, 2 of 4 (3% faster than 3 of 4)
+    constexpr int kDmaA = ((DS <= 128 ? 4 : 5) * G::NI + 7) / 8;
     // Separate LDS objects, so that the compiler can tell the chunk being read
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
