@@ -161,7 +161,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
     }
-    const bool has_bias = a.bias != nullptr;
+    const bool has_bias = (MODE == LOCAL && EXT) || a.bias != nullptr;  // the bias variant always has one
 
     ChunkStream<DS> stream;
     stream.init(d, js, lane);
@@ -175,12 +175,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (!LL && w == 0 && lane < YC) {
             // the 16 per-token records of the chunk
             const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
-            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, lane * 16);
+            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, yy * 16);
         }
         if (BZ && has_bias && w == 0 && lane < YC) {
             // the 16 biases of the chunk (zeros past the vocabulary)
             const unsigned rem = rows > 0 ? (unsigned)rows * 4u : 0u;
-            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, lane * 4);
+            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, yy * 4);
         }
     };
     issue_side(0, recA_u);
@@ -250,12 +250,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // whose stream is spread over the products and the end of the
         // elementwise step, so that neither the texture unit's queue nor the
         // LDS write port sees the whole chunk at once.
-        // (the bias variant at the widest slices holds 5 of them at a time:
-        // each later read refills the registers of the products just issued)
-        constexpr int RA = (BZ && MODE == LOCAL && G::NK > 5) ? 5 : G::NK;
-        bf16x8 ay[RA];
+        bf16x8 ay[G::NK];
 #pragma unroll
-        for (int kk = 0; kk < RA; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
+        for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
         if (more) issue_side(y0 + YC, side_nxt);
         f32x4 S[G::NXB];
 #pragma unroll
@@ -263,8 +260,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
 #pragma unroll
-            for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay[kk % RA], xr[xb][kk], S[xb]);
-            if (kk + RA < G::NK) ay[kk % RA] = *(LDS_AS bf16x8*)(cur + a_off + 64 * (kk + RA));
+            for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay[kk], xr[xb][kk], S[xb]);
             if (kk < kDmaA) {
                 if (more) stream.issue_one(nrs, d, nxt, kk);
                 __builtin_amdgcn_sched_barrier(0);  // keeps the instruction between these products
