@@ -267,17 +267,31 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
         }
         const int yg = y0 + yy;
+        // Passes without a second product at two exchange rounds: the second
+        // round's partials go into this wave's own slice of the current chunk,
+        // which no other wave reads and whose row-wise reads have returned
+        // (LDS operations of a wave run in order); the chunk buffer is next
+        // written by the stream of the chunk after next, behind this step's
+        // last barrier.  Both rounds then meet behind one barrier.
+        constexpr bool FOLD = !PC && G::NX == 2;
+        static_assert(!FOLD || PR * PP * 4 <= G::SLICE, "a round of partials fits a wave's chunk slice");
+        LDS_AS float* const slices0 = (LDS_AS float*)(LDS_AS void*)(cur - w * G::SLICE);
 #pragma unroll
         for (int rr = 0; rr < G::NX; ++rr) {
             // exchange round rr: the partials of stationary rows [rr PR, (rr + 1) PR)
-            if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
-            // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
+            if (!FOLD || rr == 0) {
+                if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
+                // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
-            for (int xb = rr * (G::NXB / G::NX); xb < (rr + 1) * (G::NXB / G::NX); ++xb) {
-                const int xl = 16 * xb - PR * rr + (lane & 15);
-                *(f32x4*)(part + (w * PR + xl) * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) = S[xb];
+                for (int xb = rr * (G::NXB / G::NX); xb < (FOLD ? G::NXB : (rr + 1) * (G::NXB / G::NX)); ++xb) {
+                    const int ro = FOLD ? xb / (G::NXB / G::NX) : rr;  // the round of this block
+                    const int xl = 16 * xb - PR * ro + (lane & 15);
+                    LDS_AS float* dst = (FOLD && ro == 1) ? slices0 + w * (G::SLICE / 4)
+                                                          : (LDS_AS float*)(LDS_AS void*)part + w * PR * PP;
+                    *(LDS_AS f32x4*)(dst + xl * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) = S[xb];
+                }
+                lds_barrier();
             }
-            lds_barrier();
 
             // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
 #pragma unroll
@@ -286,7 +300,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 const int xl = xo[r] - PR * rr;
                 const int yq = yy ^ (4 * ((xl >> 1) & 3));
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * PR + xl) * PP + yq];
+                for (int ww = 0; ww < NW; ++ww)
+                    q[ww] = (FOLD && rr == 1) ? slices0[ww * (G::SLICE / 4) + xl * PP + yq]
+                                              : ((LDS_AS float*)(LDS_AS void*)part)[(ww * PR + xl) * PP + yq];
                 static_assert(NW == 8, "partial-sum tree");
                 const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
                 float gval = 0.f;
