@@ -103,9 +103,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
     // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
     // the logit products, [kDmaA, NI) after the elementwise step.  Measured:
-    // at d = 2048, 5 of 8 inside the products (3 and 8 are 3-5% slower, 4 and 6
-    // within box-to-box noise); at d = 1024, 2 of 4 (3% faster than 3 of 4)
-    constexpr int kDmaA = ((DS <= 128 ? 4 : 5) * G::NI + 7) / 8;
+    // with a second product, at d = 2048 5 of 8 inside the products (3 and 8
+    // are 3-5% slower, 4 and 6 within box-to-box noise), at d = 1024 2 of 4 (3%
+    // faster than 3 of 4); without one (64-row tiles, twice the products per
+    // chunk) all of them, 12-14% faster than 5 of 8 at d = 2048
+    constexpr int kDmaA = PC ? ((DS <= 128 ? 4 : 5) * G::NI + 7) / 8 : G::NI;
     // Separate LDS objects, so that the compiler can tell the chunk being read
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
