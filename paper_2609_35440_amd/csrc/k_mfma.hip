@@ -249,9 +249,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 
         // ---- split-K partial of the logit tile S[y][x] over this wave's columns.
         // All operand reads go out first, ahead of the data of the next chunk,
-        // whose stream is spread over the products and the end of the
-        // elementwise step, so that neither the texture unit's queue nor the
-        // LDS write port sees the whole chunk at once.
+        // whose stream is spread over the products (and, in the passes with a
+        // second product, the end of the elementwise step), so that neither the
+        // texture unit's queue nor the LDS write port sees the whole chunk at once.
         bf16x8 ay[G::NK];
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
