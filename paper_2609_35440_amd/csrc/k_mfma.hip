@@ -75,8 +75,13 @@ struct Geo : layout::Geo<DS> {
     static constexpr int PR = (XR == 64 && DS > 128) ? 32 : XR;
     static constexpr int NX = XR / PR;                 // exchange rounds per chunk
     static constexpr int NXB = XR / 16;                // 16-row blocks of the logit product
-    static constexpr int NR = XR / 32;                 // rows per lane in the elementwise step = 32-row
-                                                       // halves of the second product
+    static constexpr int NR = XR / 32;                 // 32-row halves of the second product
+    // elementwise step: a lane takes EWC adjacent streamed columns of ER
+    // stationary rows, LPR lanes share a row (64-row tiles exchanged in one
+    // round: one row and two columns per lane)
+    static constexpr int EWC = (XR == 64 && NX == 1) ? 2 : 1;
+    static constexpr int ER = NR / EWC;
+    static constexpr int LPR = 16 / EWC;
     static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
     static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
     static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
@@ -144,16 +149,19 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     LDS_AS char* sliceB = (LDS_AS char*)(LDS_AS void*)ybufB + w * G::SLICE;
 
     // per-lane scalars of the rows this wave finishes in the elementwise step:
-    // stationary rows xo[r] = 4 w + lane/16 + 32 r, streamed row yy of the chunk
-    int xo[NR];
+    // stationary rows xo[r] = 4 w + lane/16 + 32 r and streamed column yy of
+    // the chunk, or, two columns per lane, row 8 w + lane/8 and columns yy, yy + 1
+    constexpr int EWC = G::EWC, ER = G::ER, LPR = G::LPR;
+    int xo[ER];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) xo[r] = 4 * w + (lane >> 4) + 32 * r;
-    const int yy = lane & 15;
-    float own_r2[NR];  // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
-    int own_tgt[NR];   // LL: target of row xo
-    float bx2[NR];     // readout-/bias-gradient passes: bias of the stationary readout row, base 2
+    for (int r = 0; r < ER; ++r) xo[r] = EWC == 2 ? 8 * w + (lane >> 3) : 4 * w + (lane >> 4) + 32 * r;
+    const int yy = EWC == 2 ? 2 * (lane & 7) : (lane & 15);
+    const int lane16 = lane & 15;  // the 16 lanes that stream a chunk's side data
+    float own_r2[ER];  // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
+    int own_tgt[ER];   // LL: target of row xo
+    float bx2[ER];     // readout-/bias-gradient passes: bias of the stationary readout row, base 2
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
+    for (int r = 0; r < ER; ++r) {
         own_r2[r] = 0.f;
         own_tgt[r] = -1;
         bx2[r] = 0.f;
@@ -177,12 +185,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         if (!LL && w == 0 && lane < YC) {
             // the 16 per-token records of the chunk
             const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
-            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, yy * 16);
+            buffer_load_lds16(make_rsrc(a.rowrec + 4 * (modoff + y0), rem), dst, lane16 * 16);
         }
         if (BZ && has_bias && w == 0 && lane < YC) {
             // the 16 biases of the chunk (zeros past the vocabulary)
             const unsigned rem = rows > 0 ? (unsigned)rows * 4u : 0u;
-            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, yy * 4);
+            buffer_load_lds4(make_rsrc(a.bias + (long long)k * a.V + y0, rem), dst, lane16 * 4);
         }
     };
     issue_side(0, recA_u);
@@ -224,12 +232,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int i = 0; i < 16; ++i) acc[b][h][i] = 0.f;
 
     // online softmax state (LL, base 2), per lane and row r: row xo[r], streamed column yy
-    float m_run[NR], s_part[NR], zy_part[NR];
-    float best[NR];   // EVAL: largest logit seen by this lane, and its column
-    int best_v[NR];
-    float db_part[NR];  // RGRAD / BGRAD: sum_t (p - onehot) for row xo[r]
+    float m_run[ER], s_part[ER], zy_part[ER];
+    float best[ER];   // EVAL: largest logit seen by this lane, and its column
+    int best_v[ER];
+    float db_part[ER];  // RGRAD / BGRAD: sum_t (p - onehot) for row xo[r]
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
+    for (int r = 0; r < ER; ++r) {
         m_run[r] = -INFINITY;
         s_part[r] = zy_part[r] = db_part[r] = 0.f;
         best[r] = -INFINITY;
@@ -295,54 +303,88 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 lds_barrier();
             }
 
-            // ---- elementwise step for rows xo[r] = 4w + lane/16 + 32 r (lane: row xo[r], column yy)
+            // ---- elementwise step for rows xo[r] (lane: row xo[r], columns yy .. yy + EWC - 1)
 #pragma unroll
-            for (int r = rr * (NR / G::NX); r < (rr + 1) * (NR / G::NX); ++r) {
-                float q[NW];
+            for (int r = rr * (ER / G::NX); r < (rr + 1) * (ER / G::NX); ++r) {
+                float q[EWC][NW];
                 const int xl = xo[r] - PR * rr;
-                const int yq = yy ^ (4 * ((xl >> 1) & 3));
+                const int yq = yy ^ (4 * ((xl >> 1) & 3));  // (yy even for two columns: both in one group)
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww)
-                    q[ww] = (FOLD && rr == 1) ? slices0[ww * (G::SLICE / 4) + xl * PP + yq]
-                                              : ((LDS_AS float*)(LDS_AS void*)part)[(ww * PR + xl) * PP + yq];
+                for (int ww = 0; ww < NW; ++ww) {
+                    if constexpr (EWC == 2) {
+                        const f32x2 v = *(LDS_AS f32x2*)((LDS_AS float*)(LDS_AS void*)part + (ww * PR + xl) * PP + yq);
+                        q[0][ww] = v[0];
+                        q[EWC - 1][ww] = v[1];
+                    } else {
+                        q[0][ww] = (FOLD && rr == 1) ? slices0[ww * (G::SLICE / 4) + xl * PP + yq]
+                                                     : ((LDS_AS float*)(LDS_AS void*)part)[(ww * PR + xl) * PP + yq];
+                    }
+                }
                 static_assert(NW == 8, "partial-sum tree");
-                const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
-                float gval = 0.f;
+                float sxy[EWC], gval[EWC];
+#pragma unroll
+                for (int e = 0; e < EWC; ++e) {
+                    sxy[e] = ((q[e][0] + q[e][1]) + (q[e][2] + q[e][3])) + ((q[e][4] + q[e][5]) + (q[e][6] + q[e][7]));
+                    gval[e] = 0.f;
+                }
                 if (LL) {
                     // columns past the end of the vocabulary get z = -inf (an additive
                     // mask rather than a branch, so the partial reads stay unconditional)
-                    float ymask = (yg < nY) ? 0.f : -INFINITY;
-                    if (BZ && has_bias) ymask += side[yy] * kLog2e;
-                    const float zc = __builtin_fmaf(sxy, own_r2[r], ymask);
+                    float zc[EWC];
+                    float zmax = -INFINITY;
+#pragma unroll
+                    for (int e = 0; e < EWC; ++e) {
+                        float ymask = (yg + e < nY) ? 0.f : -INFINITY;
+                        if (BZ && has_bias) ymask += side[yy + e] * kLog2e;
+                        zc[e] = __builtin_fmaf(sxy[e], own_r2[r], ymask);
+                        zmax = fmaxf(zmax, zc[e]);
+                    }
                     float alpha = 1.f;
-                    if (__builtin_expect(__any(zc > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
-                        const float cmax = row16_max(zc);
+                    if (__builtin_expect(__any(zmax > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
+                        const float cmax = group_max<LPR>(zmax);
                         if (cmax > m_run[r] + kLazyThresh2) {
                             alpha = __builtin_amdgcn_exp2f(m_run[r] - cmax);
                             s_part[r] *= alpha;
                             m_run[r] = cmax;
                         }
                     }
-                    const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
-                    s_part[r] += p;
-                    if (yg == own_tgt[r]) zy_part[r] = zc;
-                    if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
-                        best[r] = zc;
-                        best_v[r] = yg;
+#pragma unroll
+                    for (int e = 0; e < EWC; ++e) {
+                        const float p = __builtin_amdgcn_exp2f(zc[e] - m_run[r]);
+                        s_part[r] += p;
+                        if (yg + e == own_tgt[r]) zy_part[r] = zc[e];
+                        if (MODE == EVAL && zc[e] > best[r]) {  // strict: the first (lowest) column keeps a tie
+                            best[r] = zc[e];
+                            best_v[r] = yg + e;
+                        }
+                        gval[e] = p;
                     }
-                    gval = p;
-                    if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
+                    if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the lanes of a row store the same value
                 } else {
-                    // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
-                    // the end of the module read as zeros and are masked
-                    const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
-                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
-                    // (a padded token's zero record would match readout row 0 as its target)
-                    const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
-                    gval = dlt * r4[3];
-                    db_part[r] += dlt;
+#pragma unroll
+                    for (int e = 0; e < EWC; ++e) {
+                        // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
+                        // the end of the module read as zeros and are masked
+                        const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * (yy + e));
+                        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy[e], r4[1], bx2[r] - r4[0]));
+                        // (a padded token's zero record would match readout row 0 as its target)
+                        const float dlt =
+                            (yg + e < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
+                        gval[e] = dlt * r4[3];
+                        db_part[r] += dlt;
+                    }
                 }
-                if (PC) gbuf[xo[r] * YC + (yy ^ (8 * ((xo[r] >> 2) & 1)))] = (bf16)gval;
+                if (PC) {
+                    bf16* gp = gbuf + xo[r] * YC + (yy ^ (8 * ((xo[r] >> 2) & 1)));
+                    if constexpr (EWC == 2) {
+                        bf16x2 g2;
+                        g2[0] = (bf16)gval[0];
+                        g2[1] = (bf16)gval[EWC - 1];
+                        *(bf16x2*)gp = g2;
+                    } else {
+                        *gp = (bf16)gval[0];
+                    }
+                }
             }
         }
         if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
@@ -400,15 +442,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     if (LL) {
         // finish the online softmax of rows xo[r]
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            const float s = row16_sum(s_part[r]);
-            const float zy = row16_sum(zy_part[r]);
+        for (int r = 0; r < ER; ++r) {
+            const float s = group_sum<LPR>(s_part[r]);
+            const float zy = group_sum<LPR>(zy_part[r]);
             float bst = best[r];
             int bv = best_v[r];
             if (MODE == EVAL) {
-                // argmax over the 16 lanes of the row: larger logit, then lower column
+                // argmax over the lanes of the row: larger logit, then lower column
 #pragma unroll
-                for (int off = 1; off < 16; off <<= 1) {
+                for (int off = 1; off < LPR; off <<= 1) {
                     const float ob = __shfl_xor(bst, off, 64);
                     const int ov = __shfl_xor(bv, off, 64);
                     if (ob > bst || (ob == bst && (unsigned)ov < (unsigned)bv)) {
@@ -417,7 +459,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     }
                 }
             }
-            if (yy == 0) {
+            if (lane % LPR == 0) {
                 const int xr_ = x0 + xo[r];
                 const float r_row = (xr_ < nX) ? a.rstd[modoff + xr_] : 0.f;
                 const float lse2 = m_run[r] + __log2f(s);
@@ -554,11 +596,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
     }
     if (!LL) {
-        // bias gradient of the stationary readout rows: sum over the 16 lanes of the row
+        // bias gradient of the stationary readout rows: sum over the lanes of the row
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
-            const float db = row16_sum(db_part[r]);
-            if (a.dbias && yy == 0 && x0 + xo[r] < nX) a.dbias[(long long)k * a.V + x0 + xo[r]] = db * a.inv_T;
+        for (int r = 0; r < ER; ++r) {
+            const float db = group_sum<LPR>(db_part[r]);
+            if (a.dbias && lane % LPR == 0 && x0 + xo[r] < nX)
+                a.dbias[(long long)k * a.V + x0 + xo[r]] = db * a.inv_T;
         }
     }
     if (MODE == RGRAD) {

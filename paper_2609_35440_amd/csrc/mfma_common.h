@@ -11,7 +11,9 @@ namespace mfma {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -91,6 +93,31 @@ __device__ __forceinline__ float row16_sum(float x) {
     x += dpp_f<0x124>(x);
     x += dpp_f<0x128>(x);
     return x;
+}
+
+// The same over each group of 8 lanes (quad permutations, then the mirror
+// inside each half row), and the choice between the two by group size.
+__device__ __forceinline__ float row8_max(float x) {
+    x = fmaxf(x, dpp_f<0xB1>(x));   // quad_perm [1,0,3,2]
+    x = fmaxf(x, dpp_f<0x4E>(x));   // quad_perm [2,3,0,1]
+    x = fmaxf(x, dpp_f<0x141>(x));  // row_half_mirror
+    return x;
+}
+__device__ __forceinline__ float row8_sum(float x) {
+    x += dpp_f<0xB1>(x);
+    x += dpp_f<0x4E>(x);
+    x += dpp_f<0x141>(x);
+    return x;
+}
+template <int N>
+__device__ __forceinline__ float group_max(float x) {
+    static_assert(N == 8 || N == 16, "lane groups of 8 or 16");
+    return N == 16 ? row16_max(x) : row8_max(x);
+}
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+    static_assert(N == 8 || N == 16, "lane groups of 8 or 16");
+    return N == 16 ? row16_sum(x) : row8_sum(x);
 }
 
 __device__ __forceinline__ unsigned lds_addr(LDS_AS char* p) {
