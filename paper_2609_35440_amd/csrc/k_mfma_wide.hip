@@ -6,9 +6,11 @@
 // with the bias of Algorithm 1):  z_tv = tau_k r_t <R_kv, g_k * h_t> + b_kv.
 // What the width changes is what fits on a CU:
 //
-//   - 16 stationary rows per workgroup instead of 32: wave w owns the d/8
-//     columns [w d/8, (w+1) d/8) of a 16 x d/8 fp32 accumulator (80 registers
-//     per lane at d = 2560) and of the stationary operand;
+//   - 16 stationary rows per workgroup in the passes with a second product:
+//     wave w owns the d/8 columns [w d/8, (w+1) d/8) of a 16 x d/8 fp32
+//     accumulator (80 registers per lane at d = 2560) and of the stationary
+//     operand; the passes without one (exit evaluation, bias gradient) hold
+//     32 stationary rows, two 16-row blocks of the logit product;
 //   - the second product runs on the 16x16x16 instruction (its contraction
 //     over the 16 streamed rows of a chunk), its streamed operand read with
 //     one ds_read_b64_tr_b16 per product;
@@ -19,8 +21,8 @@
 //     to LDS once the current chunk's last read has returned.
 //
 // Per chunk each wave (1) reads its slice row-wise and computes its split-K
-// partial of the 16x16 logit tile; (2) the 8 partials meet in LDS and each
-// wave finishes the elementwise step for 2 of the 16 stationary rows;
+// partial of the 16 x XR logit tile; (2) the 8 partials meet in LDS and each
+// wave finishes the elementwise step for XR / 8 of the stationary rows;
 // (3) every wave accumulates its column slice of the second product; then
 // (4) it writes the staged next chunk into its slice and stages the one after.
 #include "mfma_common.h"
@@ -34,7 +36,6 @@ using namespace mfma;
 
 constexpr int NW = layoutw::NW;  // waves per workgroup
 constexpr int NTHR = NW * 64;
-constexpr int XR = kMfmaWideRows;  // stationary rows per workgroup (16)
 constexpr int YC = layoutw::YC;    // streamed rows per chunk
 // Partial logit tiles part[w][x][y]: rows of PP = 16 floats, the 16-byte
 // group y / 4 of row x stored at (y / 4) ^ ((x >> 1) & 3): conflict-free
@@ -43,11 +44,17 @@ constexpr int YC = layoutw::YC;    // streamed rows per chunk
 // so that the 8-byte reads of its 16 rows spread over all 64 banks.
 constexpr int PP = 16;
 
-static_assert(XR == 16, "one 16-row block of stationary rows");
+// Stationary rows per workgroup: 16 in the passes with a second product (the
+// accumulator and the stationary operand fill the register file), 32 in the
+// passes without one (exit evaluation, bias gradient), which halves the
+// readout streamed per flop.
+template <bool PC>
+constexpr int wide_rows() { return PC ? kMfmaWideRows : 32; }
+static_assert(kMfmaWideRows == 16, "one 16-row block of stationary rows with a second product");
 
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
 
-template <int DS>
+template <int DS, int XR>
 struct Geo : layoutw::Geo<DS> {
     static constexpr int NK = DS / 32;  // 32-deep k-steps of the logit product
     static constexpr int NB = DS / 16;  // 16-column accumulator blocks per wave
@@ -66,14 +73,17 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
     return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
 }
 
-// MODE LOCAL / EVAL: grid (ceil(T/16), K); module k = blockIdx.y.
-// MODE RGRAD / BGRAD: grid (ceil(V/16), nmod); module k = m0 + blockIdx.y.
+// MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
+// MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
+// XR = 16 with a second product (LOCAL, RGRAD), 32 without (EVAL, BGRAD).
 // EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
-    using G = Geo<DS>;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;           // X = h, Y = readout
     constexpr bool PC = MODE == LOCAL || MODE == RGRAD;          // second product
+    constexpr int XR = wide_rows<PC>();
+    constexpr int NXB = XR / 16;                                 // 16-row blocks of the logit product
+    using G = Geo<DS, XR>;
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
     constexpr int RA = 4;                                        // row-wise reads in flight
     __shared__ __attribute__((aligned(16))) char ybuf[G::YBUF];
@@ -105,11 +115,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 
     LDS_AS char* slice = (LDS_AS char*)(LDS_AS void*)ybuf + w * G::SLICE;
 
-    // elementwise ownership: lanes l and l + 32 both compute stationary row
-    // xo, streamed column yy; only l < 32 writes
-    const int xo = 2 * w + ((lane >> 4) & 1);
+    // elementwise ownership: stationary row xo, streamed column yy.  With 16
+    // rows lanes l and l + 32 both compute row xo and only l < 32 writes; with
+    // 32 rows every lane has its own element
+    const int xo = XR == 16 ? 2 * w + ((lane >> 4) & 1) : 4 * w + (lane >> 4);
     const int yy = lane & 15;
-    const bool wr = lane < 32;
+    const bool wr = XR == 32 || lane < 32;
     float own_r2 = 0.f;  // LL: r_t tau_k log2 e of row xo
     int own_tgt = -1;    // LL: target of row xo
     if (LL && x0 + xo < nX) {
@@ -164,25 +175,28 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 
     // stationary operand (local loss and exit evaluation: times the gain,
     // rounded once): B of the 16x16x32 logit product, lane holds
-    // X[x0 + lane%16][js + 32 kk + 8 (lane/16) .. +7]
-    bf16x8 xr[G::NK];
+    // X[x0 + 16 xb + lane%16][js + 32 kk + 8 (lane/16) .. +7]
+    bf16x8 xr[NXB][G::NK];
 #pragma unroll
     for (int kk = 0; kk < G::NK; ++kk) {
         const int j0 = js + 32 * kk + 8 * (lane >> 4);
         const bf16x8 gv = *(const bf16x8*)(gk + j0);
-        const int xrow = x0 + (lane & 15);
-        bf16x8 xv;
-        if (xrow < nX) {
-            xv = *(const bf16x8*)(X + (long long)xrow * d + j0);
-        } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) xv[e] = (bf16)0.f;
-        }
-        if (LL) {
+        for (int xb = 0; xb < NXB; ++xb) {
+            const int xrow = x0 + 16 * xb + (lane & 15);
+            bf16x8 xv;
+            if (xrow < nX) {
+                xv = *(const bf16x8*)(X + (long long)xrow * d + j0);
+            } else {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) xr[kk][e] = (bf16)((float)xv[e] * (float)gv[e]);
-        } else {
-            xr[kk] = xv;
+                for (int e = 0; e < 8; ++e) xv[e] = (bf16)0.f;
+            }
+            if (LL) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) xr[xb][kk][e] = (bf16)((float)xv[e] * (float)gv[e]);
+            } else {
+                xr[xb][kk] = xv;
+            }
         }
     }
 
@@ -211,19 +225,26 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         for (int kk = 0; kk < RA && kk < G::NK; ++kk)
             ay[kk] = *(LDS_AS bf16x8*)(slice + ((kk & 1) ? rd_odd : rd_even) + 64 * kk);
         if (more) issue_side(y0 + YC, side_nxt);
-        f32x4 S0 = {0.f, 0.f, 0.f, 0.f};
+        f32x4 S[NXB];
+#pragma unroll
+        for (int xb = 0; xb < NXB; ++xb) S[xb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
             const bf16x8 wa = ay[kk % RA];
             if (kk + RA < G::NK)
                 ay[kk % RA] = *(LDS_AS bf16x8*)(slice + (((kk + RA) & 1) ? rd_odd : rd_even) + 64 * (kk + RA));
-            S0 = mfma16(wa, xr[kk], S0);
+#pragma unroll
+            for (int xb = 0; xb < NXB; ++xb) S[xb] = mfma16(wa, xr[xb][kk], S[xb]);
         }
-        // C layout: lane holds S[y = 4 (lane/16) + i][x = lane%16]; store as part[w][x][y]
-        *(f32x4*)(part + (w * XR + (lane & 15)) * PP + 4 * ((lane >> 4) ^ (((lane & 15) >> 1) & 3))) = S0;
+        // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
+#pragma unroll
+        for (int xb = 0; xb < NXB; ++xb) {
+            const int xl = 16 * xb + (lane & 15);
+            *(f32x4*)(part + (w * XR + xl) * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) = S[xb];
+        }
         lds_barrier();
 
-        // ---- (2) elementwise step for rows xo = 2w, 2w+1 (lane: row xo, column yy)
+        // ---- (2) elementwise step (lane: row xo, column yy)
         float q[NW];
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + (yy ^ (4 * ((xo >> 1) & 3)))];
@@ -306,7 +327,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     const int ex = lane & 15;
     const int eg = lane >> 4;
     if (LL) {
-        // finish the online softmax of rows 2w, 2w+1
+        // finish the online softmax of row xo
         const float s = row16_sum(s_part);
         const float zy = row16_sum(zy_part);
         if (MODE == EVAL) {
@@ -431,6 +452,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 template <int MODE, int DS, bool EXT>
 hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
     const bool ll = MODE == LOCAL || MODE == EVAL;
+    constexpr int XR = wide_rows<MODE == LOCAL || MODE == RGRAD>();
     dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
                    : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused_wide<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
