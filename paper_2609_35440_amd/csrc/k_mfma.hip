@@ -29,7 +29,7 @@
 //   bias-gradient pass: the readout-gradient pass without the second product,
 //     for modules whose bias is trained but whose readout is not.
 //
-// Work split: a workgroup of 8 waves owns XR stationary rows (32, or 64 where
+// Work split: a workgroup of 8 waves owns XR stationary rows (32, 64 or 128 where
 // the register file allows it: see rows_of); wave w owns the d/8 columns
 // [w d/8, (w+1) d/8).  Per chunk of 16 streamed rows, every wave multiplies
 // its column slice (split-K partial of the logit tile), the partials meet in
@@ -61,11 +61,12 @@ constexpr int PP = 16;
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
 
 // Stationary rows per workgroup: 64 while the accumulator (64 rows x d/8
-// columns) and the stationary operand fit the register file (d <= 1024), or
-// in the passes without a second product (no accumulator) up to d = 2048; 32
-// otherwise.  The readout streamed per flop halves with the taller tile.
+// columns) and the stationary operand fit the register file (d <= 1024), 32
+// otherwise.  The passes without a second product (no accumulator) hold as
+// many rows as 128 registers of stationary operand take: 128 up to d = 1024,
+// 64 at d = 2048.  The readout streamed per flop halves with each doubling.
 template <int DS, bool PC>
-constexpr int rows_of() { return (DS <= 128 || (!PC && DS <= 256)) ? 64 : 32; }
+constexpr int rows_of() { return (!PC && DS <= 128) ? 128 : ((DS <= 128 || (!PC && DS <= 256)) ? 64 : 32); }
 
 template <int DS, bool PC>
 struct Geo : layout::Geo<DS> {

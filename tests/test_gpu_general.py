@@ -24,6 +24,8 @@ CASES = [
      dict(final_module_dW=True, want_dtau=True)),
     ("mfma_d512_bias_only_frozen_heads", "340m", dict(K=3, T=45, d=512, V=97),
      dict(wbar="per_head", bias=True), dict(final_module_dW=True, want_dbias=True)),
+    ("mfma_d256_bias_grad_three_tiles", "340m", dict(K=2, T=70, d=256, V=300), dict(bias=True),
+     dict(final_module_dW=True, want_dbias=True)),
     ("mfma_d768_priv_without_terminal", "340m", dict(K=3, T=50, d=768, V=150), ALL,
      dict(final_module_dW=False, heads_train_readout=True, want_dtau=True, want_dbias=True)),
     ("mfma_d2048_per_module_gain_frozen", "1b", dict(K=3, T=40, d=2048, V=100), dict(per_module_gain=True),
@@ -185,6 +187,7 @@ EVAL_CASES = [
     ("mfma_d2048", "1b", dict(K=3, T=65, d=2048, V=515), ALL),
     ("mfma_d256_plain", "340m", dict(K=2, T=70, d=256, V=300), dict()),
     ("mfma_d1024_shared", "340m", dict(K=3, T=40, d=1024, V=1000), dict(wbar="shared", tau=True)),
+    ("mfma_d512_three_tiles", "340m", dict(K=2, T=300, d=512, V=211), dict(tau=True, bias=True)),
     ("wide_d2560", "2b", dict(K=3, T=37, d=2560, V=300), ALL),
     ("valu_f32", "tiny", dict(K=3, T=37, d=24, V=45), ALL),
     ("valu_bf16_d72", "340m", dict(K=2, T=10, d=72, V=50), ALL),
