@@ -91,7 +91,7 @@ size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int fi
  * Name of the kernel family one call with these sizes runs on:
  * "mfma" (bf16 matrix-core kernels: d a multiple of 256 up to 2048; tiles of
  * 64 rows up to d = 1024 and 32 above, twice that in the forward-only
- * passes), "mfma_wide" (bf16 matrix-core kernels, d = 2560; 16-row tiles, 32
+ * passes), "mfma_wide" (bf16 matrix-core kernels, d = 2560; 16-row tiles, 48
  * in the forward-only passes) or
  * "valu" (fp32 vector-ALU kernels, used for SOLO_F32 and for every other bf16
  * width).  Returns "invalid" for arguments solo_readout_fwd_bwd would reject.

@@ -10,7 +10,7 @@
 //     wave w owns the d/8 columns [w d/8, (w+1) d/8) of a 16 x d/8 fp32
 //     accumulator (80 registers per lane at d = 2560) and of the stationary
 //     operand; the passes without one (exit evaluation, bias gradient) hold
-//     32 stationary rows, two 16-row blocks of the logit product;
+//     48 stationary rows, three 16-row blocks of the logit product;
 //   - the second product runs on the 16x16x16 instruction (its contraction
 //     over the 16 streamed rows of a chunk), its streamed operand read with
 //     one ds_read_b64_tr_b16 per product;
@@ -45,11 +45,11 @@ constexpr int YC = layoutw::YC;    // streamed rows per chunk
 constexpr int PP = 16;
 
 // Stationary rows per workgroup: 16 in the passes with a second product (the
-// accumulator and the stationary operand fill the register file), 32 in the
-// passes without one (exit evaluation, bias gradient), which halves the
-// readout streamed per flop.
+// accumulator and the stationary operand fill the register file), 48 in the
+// passes without one (exit evaluation, bias gradient: 120 registers of
+// stationary operand), which cuts the readout streamed per flop to a third.
 template <bool PC>
-constexpr int wide_rows() { return PC ? kMfmaWideRows : 32; }
+constexpr int wide_rows() { return PC ? kMfmaWideRows : 48; }
 static_assert(kMfmaWideRows == 16, "one 16-row block of stationary rows with a second product");
 
 enum Mode { LOCAL = 0, RGRAD = 1, BGRAD = 2, EVAL = 3 };
@@ -75,7 +75,7 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
 
 // MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
 // MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
-// XR = 16 with a second product (LOCAL, RGRAD), 32 without (EVAL, BGRAD).
+// XR = 16 with a second product (LOCAL, RGRAD), 48 without (EVAL, BGRAD).
 // EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
@@ -83,6 +83,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     constexpr bool PC = MODE == LOCAL || MODE == RGRAD;          // second product
     constexpr int XR = wide_rows<PC>();
     constexpr int NXB = XR / 16;                                 // 16-row blocks of the logit product
+    static_assert((PC && XR == 16) || (!PC && (XR == 16 || XR == 32 || XR == 48)), "tile height");
     using G = Geo<DS, XR>;
     constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
     constexpr int RA = 4;                                        // row-wise reads in flight
@@ -115,21 +116,36 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 
     LDS_AS char* slice = (LDS_AS char*)(LDS_AS void*)ybuf + w * G::SLICE;
 
-    // elementwise ownership: stationary row xo, streamed column yy.  With 16
-    // rows lanes l and l + 32 both compute row xo and only l < 32 writes; with
-    // 32 rows every lane has its own element
-    const int xo = XR == 16 ? 2 * w + ((lane >> 4) & 1) : 4 * w + (lane >> 4);
-    const int yy = lane & 15;
-    const bool wr = XR == 32 || lane < 32;
-    float own_r2 = 0.f;  // LL: r_t tau_k log2 e of row xo
-    int own_tgt = -1;    // LL: target of row xo
-    if (LL && x0 + xo < nX) {
-        own_r2 = a.rstd[modoff + x0 + xo] * tau_k * kLog2e;
-        own_tgt = a.targets[modoff + x0 + xo];
+    // elementwise ownership: the lane finishes stationary rows xo[r], r < ER,
+    // at streamed column yy; only lanes with wr[r] write row xo[r].  16 rows:
+    // row 2w + (l/16)%2, computed by lanes l and l + 32, written by l < 32;
+    // 32 rows: row 4w + l/16; 48 rows: rows 6w + l/16 and 6w + 4 + (l/16)%2,
+    // the second one again computed twice and written by l < 32
+    constexpr int ER = XR == 48 ? 2 : 1;
+    int xo[ER];
+    bool wr[ER];
+    xo[0] = XR == 16 ? 2 * w + ((lane >> 4) & 1) : (XR == 32 ? 4 * w : 6 * w) + (lane >> 4);
+    wr[0] = XR != 16 || lane < 32;
+    if constexpr (ER == 2) {
+        xo[ER - 1] = 6 * w + 4 + ((lane >> 4) & 1);
+        wr[ER - 1] = lane < 32;
     }
-    float bx2 = 0.f;  // RGRAD / BGRAD: bias of the stationary readout row, base 2
-    if (!LL && a.bias && x0 + xo < nX) bx2 = a.bias[(long long)k * a.V + x0 + xo] * kLog2e;
-    const bool has_bias = a.bias != nullptr;
+    const int yy = lane & 15;
+    float own_r2[ER];  // LL: r_t tau_k log2 e of row xo[r]
+    int own_tgt[ER];   // LL: target of row xo[r]
+    float bx2[ER];     // RGRAD / BGRAD: bias of the stationary readout row, base 2
+#pragma unroll
+    for (int r = 0; r < ER; ++r) {
+        own_r2[r] = 0.f;
+        own_tgt[r] = -1;
+        bx2[r] = 0.f;
+        if (LL && x0 + xo[r] < nX) {
+            own_r2[r] = a.rstd[modoff + x0 + xo[r]] * tau_k * kLog2e;
+            own_tgt[r] = a.targets[modoff + x0 + xo[r]];
+        }
+        if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
+    }
+    const bool has_bias = (MODE == LOCAL && EXT) || a.bias != nullptr;  // the bias variant always has one
 
     // ---- staged stream: lane p of load q fetches slot 64 q + p of the wave's
     // slice (row-contiguous), with zeros past the last streamed row
@@ -204,11 +220,18 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 #pragma unroll
     for (int b = 0; b < (PC ? G::NB : 1); ++b) acc[b] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-    // online softmax state (LL, base 2), per lane: row xo, streamed column yy
-    float m_run = -INFINITY, s_part = 0.f, zy_part = 0.f;
-    float best = -INFINITY;  // EVAL: largest logit seen by this lane, and its column
-    int best_v = -1;
-    float db_part = 0.f;     // RGRAD / BGRAD: sum_t (p - onehot) for row xo
+    // online softmax state (LL, base 2), per lane: row xo[r], streamed column yy
+    float m_run[ER], s_part[ER], zy_part[ER];
+    float best[ER];  // EVAL: largest logit seen by this lane, and its column
+    int best_v[ER];
+    float db_part[ER];  // RGRAD / BGRAD: sum_t (p - onehot) for row xo[r]
+#pragma unroll
+    for (int r = 0; r < ER; ++r) {
+        m_run[r] = -INFINITY;
+        s_part[r] = zy_part[r] = db_part[r] = 0.f;
+        best[r] = -INFINITY;
+        best_v[r] = -1;
+    }
 
     // row-wise read of k-step kk at rd_even + 64 kk (kk even) or rd_odd + 64 kk (kk odd):
     // the swizzle flips bit 2 of the granule index for rows with (r & 4)
@@ -244,48 +267,51 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         }
         lds_barrier();
 
-        // ---- (2) elementwise step (lane: row xo, column yy)
-        float q[NW];
+        // ---- (2) elementwise step (lane: rows xo[r], column yy)
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo) * PP + (yy ^ (4 * ((xo >> 1) & 3)))];
-        static_assert(NW == 8, "partial-sum tree");
-        const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
-        const int yg = y0 + yy;
-        float gval = 0.f;
-        if (LL) {
-            // columns past the end of the vocabulary get z = -inf
-            float ymask = (yg < nY) ? 0.f : -INFINITY;
-            if (BZ && has_bias) ymask += side[yy] * kLog2e;
-            const float zc = __builtin_fmaf(sxy, own_r2, ymask);
-            float alpha = 1.f;
-            if (__builtin_expect(__any(zc > m_run + kLazyThresh2), 0)) {  // wave-uniform
-                const float cmax = row16_max(zc);
-                if (cmax > m_run + kLazyThresh2) {
-                    alpha = __builtin_amdgcn_exp2f(m_run - cmax);
-                    s_part *= alpha;
-                    m_run = cmax;
+        for (int r = 0; r < ER; ++r) {
+            float q[NW];
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) q[ww] = part[(ww * XR + xo[r]) * PP + (yy ^ (4 * ((xo[r] >> 1) & 3)))];
+            static_assert(NW == 8, "partial-sum tree");
+            const float sxy = ((q[0] + q[1]) + (q[2] + q[3])) + ((q[4] + q[5]) + (q[6] + q[7]));
+            const int yg = y0 + yy;
+            float gval = 0.f;
+            if (LL) {
+                // columns past the end of the vocabulary get z = -inf
+                float ymask = (yg < nY) ? 0.f : -INFINITY;
+                if (BZ && has_bias) ymask += side[yy] * kLog2e;
+                const float zc = __builtin_fmaf(sxy, own_r2[r], ymask);
+                float alpha = 1.f;
+                if (__builtin_expect(__any(zc > m_run[r] + kLazyThresh2), 0)) {  // wave-uniform
+                    const float cmax = row16_max(zc);
+                    if (cmax > m_run[r] + kLazyThresh2) {
+                        alpha = __builtin_amdgcn_exp2f(m_run[r] - cmax);
+                        s_part[r] *= alpha;
+                        m_run[r] = cmax;
+                    }
                 }
+                const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
+                s_part[r] += p;
+                if (yg == own_tgt[r]) zy_part[r] = zc;
+                if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
+                    best[r] = zc;
+                    best_v[r] = yg;
+                }
+                gval = p;
+                if (MODE == LOCAL && wr[r]) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
+            } else {
+                // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
+                // the end of the module read as zeros and are masked
+                const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
+                // (a padded token's zero record would match readout row 0 as its target)
+                const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
+                gval = dlt * r4[3];
+                db_part[r] += dlt;
             }
-            const float p = __builtin_amdgcn_exp2f(zc - m_run);
-            s_part += p;
-            if (yg == own_tgt) zy_part = zc;
-            if (MODE == EVAL && zc > best) {  // strict: the first (lowest) column keeps a tie
-                best = zc;
-                best_v = yg;
-            }
-            gval = p;
-            if (MODE == LOCAL && wr) abuf[xo] = alpha;  // the 16 lanes of a row store the same value
-        } else {
-            // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
-            // the end of the module read as zeros and are masked
-            const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2 - r4[0]));
-            // (a padded token's zero record would match readout row 0 as its target)
-            const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo ? 1.f : 0.f) : 0.f;
-            gval = dlt * r4[3];
-            db_part += dlt;
+            if (PC && wr[r]) gbuf[xo[r] * YC + (yy ^ (8 * ((xo[r] >> 3) & 1)))] = (bf16)gval;
         }
-        if (PC && wr) gbuf[xo * YC + (yy ^ (8 * ((xo >> 3) & 1)))] = (bf16)gval;
         lds_barrier();
 
         if (PC) {
@@ -327,37 +353,43 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     const int ex = lane & 15;
     const int eg = lane >> 4;
     if (LL) {
-        // finish the online softmax of row xo
-        const float s = row16_sum(s_part);
-        const float zy = row16_sum(zy_part);
-        if (MODE == EVAL) {
-            // argmax over the 16 lanes of the row: larger logit, then lower column
+        // finish the online softmax of rows xo[r]
 #pragma unroll
-            for (int off = 1; off < 16; off <<= 1) {
-                const float ob = __shfl_xor(best, off, 64);
-                const int ov = __shfl_xor(best_v, off, 64);
-                if (ob > best || (ob == best && (unsigned)ov < (unsigned)best_v)) {
-                    best = ob;
-                    best_v = ov;
+        for (int r = 0; r < ER; ++r) {
+            const float s = row16_sum(s_part[r]);
+            const float zy = row16_sum(zy_part[r]);
+            float bst = best[r];
+            int bv = best_v[r];
+            if (MODE == EVAL) {
+                // argmax over the 16 lanes of the row: larger logit, then lower column
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    const float ob = __shfl_xor(bst, off, 64);
+                    const int ov = __shfl_xor(bv, off, 64);
+                    if (ob > bst || (ob == bst && (unsigned)ov < (unsigned)bv)) {
+                        bst = ob;
+                        bv = ov;
+                    }
                 }
             }
-        }
-        if (yy == 0 && wr) {
-            const float r_row = (x0 + xo < nX) ? a.rstd[modoff + x0 + xo] : 0.f;
-            const float lse2 = m_run + __log2f(s);
-            const bool tok = own_tgt >= 0 && own_tgt < nY;
-            const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
-            if (x0 + xo < nX) {
-                const long long t = modoff + x0 + xo;
-                a.lse[t] = lse2 * kLn2;
-                a.rowloss[t] = rl;
-                if (MODE == EVAL && a.top1) a.top1[t] = best_v;
-                if (MODE == LOCAL && a.rowrec) {
-                    f32x4 rec4 = {lse2, own_r2, __int_as_float(own_tgt), r_row * tau_k * a.inv_T};
-                    *(f32x4*)(a.rowrec + 4 * t) = rec4;
+            if (yy == 0 && wr[r]) {
+                const int xr_ = x0 + xo[r];
+                const float r_row = (xr_ < nX) ? a.rstd[modoff + xr_] : 0.f;
+                const float lse2 = m_run[r] + __log2f(s);
+                const bool tok = own_tgt[r] >= 0 && own_tgt[r] < nY;
+                const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
+                if (xr_ < nX) {
+                    const long long t = modoff + xr_;
+                    a.lse[t] = lse2 * kLn2;
+                    a.rowloss[t] = rl;
+                    if (MODE == EVAL && a.top1) a.top1[t] = bv;
+                    if (MODE == LOCAL && a.rowrec) {
+                        f32x4 rec4 = {lse2, own_r2[r], __int_as_float(own_tgt[r]), r_row * tau_k * a.inv_T};
+                        *(f32x4*)(a.rowrec + 4 * t) = rec4;
+                    }
                 }
+                sbuf[xo[r]] = 1.f / s;
             }
-            sbuf[xo] = 1.f / s;
         }
     }
     if (MODE == LOCAL) {
@@ -435,8 +467,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     }
     if (!LL) {
         // bias gradient of the stationary readout rows: sum over the 16 lanes of the row
-        const float db = row16_sum(db_part);
-        if (a.dbias && yy == 0 && wr && x0 + xo < nX) a.dbias[(long long)k * a.V + x0 + xo] = db * a.inv_T;
+#pragma unroll
+        for (int r = 0; r < ER; ++r) {
+            const float db = row16_sum(db_part[r]);
+            if (a.dbias && yy == 0 && wr[r] && x0 + xo[r] < nX)
+                a.dbias[(long long)k * a.V + x0 + xo[r]] = db * a.inv_T;
+        }
     }
     if (MODE == RGRAD) {
         const int v = x0 + ex;
