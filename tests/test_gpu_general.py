@@ -42,6 +42,8 @@ CASES = [
      dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
     ("wide_d2560_shared_copy_bias", "2b", dict(K=3, T=20, d=2560, V=70),
      dict(wbar="shared", tau=True, bias=True), dict(final_module_dW=True, want_dtau=True, want_dbias=True)),
+    ("wide_d2560_bias_grad_V_below_tile", "2b", dict(K=2, T=20, d=2560, V=20), dict(bias=True),
+     dict(final_module_dW=True, want_dbias=True)),
     ("valu_f32_all", "tiny", dict(K=3, T=37, d=24, V=45), ALL,
      dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True)),
     ("valu_f32_shared_copy", "tiny", dict(K=2, T=20, d=64, V=33), dict(wbar="shared", tau=True, bias=True),
@@ -189,6 +191,8 @@ EVAL_CASES = [
     ("mfma_d1024_shared", "340m", dict(K=3, T=40, d=1024, V=1000), dict(wbar="shared", tau=True)),
     ("mfma_d512_three_tiles", "340m", dict(K=2, T=300, d=512, V=211), dict(tau=True, bias=True)),
     ("wide_d2560", "2b", dict(K=3, T=37, d=2560, V=300), ALL),
+    ("wide_d2560_T1", "2b", dict(K=2, T=1, d=2560, V=77), dict(tau=True, bias=True)),
+    ("wide_d2560_two_tiles", "2b", dict(K=2, T=60, d=2560, V=130), dict()),
     ("valu_f32", "tiny", dict(K=3, T=37, d=24, V=45), ALL),
     ("valu_bf16_d72", "340m", dict(K=2, T=10, d=72, V=50), ALL),
 ]
@@ -212,8 +216,16 @@ def test_exit_eval_parity(name, cfg, ov, extras):
                            bias=x.get("bias"))
     dtype = x["cfg"].dtype
     tol = TOL[dtype]
-    np.testing.assert_allclose(losses, ref["losses"], rtol=tol["loss"])
-    assert np.abs(row_loss - ref["row_loss"]).max() <= 2 * tol["loss"] * max(np.abs(ref["row_loss"]).max(), 1.0)
+    # the rounding error of a logit is tau_k times that of the product it scales (Eq. 2), so
+    # the per-token bound grows with tau_k; a module loss averages the token errors only when
+    # it has enough tokens, otherwise it is held to the per-token bound
+    tscale = np.maximum(1.0, x["tau"]) if x.get("tau") is not None else np.ones(losses.shape[0])
+    row_tol = 2 * tol["loss"] * max(np.abs(ref["row_loss"]).max(), 1.0) * tscale
+    assert np.all(np.abs(row_loss - ref["row_loss"]).max(axis=1) <= row_tol), (row_loss, ref["row_loss"])
+    if row_loss.shape[1] >= 16:
+        np.testing.assert_allclose(losses, ref["losses"], rtol=tol["loss"])
+    else:
+        assert np.all(np.abs(losses - ref["losses"]) <= row_tol), (losses, ref["losses"])
     # the top-1 is unique only up to ties and rounding: the chosen column must be a
     # maximiser of the fp64 logits within the error of the kernel's logits
     # (bf16 operands: about 2^-8 of |z|; fp32: 1e-5), and most rows agree exactly
