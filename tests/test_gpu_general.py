@@ -198,20 +198,19 @@ EVAL_CASES = [
 ]
 
 
-@pytest.mark.parametrize("name,cfg,ov,extras", EVAL_CASES, ids=[c[0] for c in EVAL_CASES])
-def test_exit_eval_parity(name, cfg, ov, extras):
+def run_exit_eval(x):
     import torch
 
     from paper_2609_35440_amd import binding
 
-    x = make_extras(make_inputs(cfg, seed=31, **ov), 31, **extras)
-    log(f"eval case {name}: {x['cfg']} extras {extras}")
     f = _dev(x)
     out = binding.exit_eval(f["h"], f["gain"], f["W"], f["targets"], Wbar=f["Wbar"], tau=f["tau"], bias=f["bias"])
     torch.cuda.synchronize()
-    losses = out.losses.double().cpu().numpy()
-    row_loss = out.row_loss.double().cpu().numpy()
-    top1 = out.top1.cpu().numpy()
+    return out.losses.double().cpu().numpy(), out.row_loss.double().cpu().numpy(), out.top1.cpu().numpy()
+
+
+def check_exit_eval(x, losses, row_loss, top1, what, min_rows_for_agreement=1):
+    """Exit-evaluation outputs against the oracle at the tolerances of the dtype."""
     ref = oracle.exit_eval(x["h"], x["gain"], x["W"], x["targets"], Wbar=x.get("Wbar"), tau=x.get("tau"),
                            bias=x.get("bias"))
     dtype = x["cfg"].dtype
@@ -221,11 +220,11 @@ def test_exit_eval_parity(name, cfg, ov, extras):
     # it has enough tokens, otherwise it is held to the per-token bound
     tscale = np.maximum(1.0, x["tau"]) if x.get("tau") is not None else np.ones(losses.shape[0])
     row_tol = 2 * tol["loss"] * max(np.abs(ref["row_loss"]).max(), 1.0) * tscale
-    assert np.all(np.abs(row_loss - ref["row_loss"]).max(axis=1) <= row_tol), (row_loss, ref["row_loss"])
+    assert np.all(np.abs(row_loss - ref["row_loss"]).max(axis=1) <= row_tol), (what, row_loss, ref["row_loss"])
     if row_loss.shape[1] >= 16:
-        np.testing.assert_allclose(losses, ref["losses"], rtol=tol["loss"])
+        np.testing.assert_allclose(losses, ref["losses"], rtol=tol["loss"], err_msg=what)
     else:
-        assert np.all(np.abs(losses - ref["losses"]) <= row_tol), (losses, ref["losses"])
+        assert np.all(np.abs(losses - ref["losses"]) <= row_tol), (what, losses, ref["losses"])
     # the top-1 is unique only up to ties and rounding: the chosen column must be a
     # maximiser of the fp64 logits within the error of the kernel's logits
     # (bf16 operands: about 2^-8 of |z|; fp32: 1e-5), and most rows agree exactly
@@ -234,16 +233,25 @@ def test_exit_eval_parity(name, cfg, ov, extras):
     for k in range(K):
         for t in range(T):
             v = int(top1[k, t])
-            assert 0 <= v < x["cfg"].V, (k, t, v)
+            assert 0 <= v < x["cfg"].V, (what, k, t, v)
             zv = ref["logits_of"](k, t, v)
-            assert zv >= ref["zmax"][k, t] - ztol_rel * (1.0 + abs(ref["zmax"][k, t])), (k, t, v, zv, ref["zmax"][k, t])
+            assert zv >= ref["zmax"][k, t] - ztol_rel * (1.0 + abs(ref["zmax"][k, t])), (what, k, t, v, zv,
+                                                                                        ref["zmax"][k, t])
     agree = float((top1 == ref["top1"]).mean())
-    log(f"{name}: top-1 agreement {agree:.4f}")
-    assert agree >= (0.95 if dtype == "bf16" else 0.99)
+    log(f"{what}: top-1 agreement {agree:.4f}")
+    if K * T >= min_rows_for_agreement:
+        assert agree >= (0.95 if dtype == "bf16" else 0.99), (what, agree)
     # the eval losses equal the training call's losses (same forward)
-    flags = dict(final_module_dW=False)
-    g = run_general(x, flags)
-    np.testing.assert_allclose(losses, g["losses"], rtol=1e-6)
+    g = run_general(x, dict(final_module_dW=False))
+    np.testing.assert_allclose(losses, g["losses"], rtol=1e-6, err_msg=what)
+
+
+@pytest.mark.parametrize("name,cfg,ov,extras", EVAL_CASES, ids=[c[0] for c in EVAL_CASES])
+def test_exit_eval_parity(name, cfg, ov, extras):
+    x = make_extras(make_inputs(cfg, seed=31, **ov), 31, **extras)
+    log(f"eval case {name}: {x['cfg']} extras {extras}")
+    losses, row_loss, top1 = run_exit_eval(x)
+    check_exit_eval(x, losses, row_loss, top1, name)
 
 
 def test_exit_eval_ties_go_to_lowest_index():

@@ -1,8 +1,9 @@
 """GPU parity on a seeded sweep of random shapes: every kernel family and
 tiling (32- and 64-row matrix-core tiles, the wide tiling, the vector-ALU
 family in bf16 and fp32), random module counts, ragged token and vocabulary
-counts, with and without the final module's readout gradient, and the general
-entry point with random option sets.  Each case is compared element by
+counts, with and without the final module's readout gradient, the general
+entry point with random option sets, and exit evaluation across the
+forward-only tilings (128, 64 and 48 rows).  Each case is compared element by
 element with the fp64 oracle at the tolerances of its dtype."""
 import zlib
 
@@ -12,7 +13,7 @@ import pytest
 import oracle
 from solo_inputs import make_extras, make_inputs
 from tests.gpu_helpers import check_close, log, run_gpu
-from tests.test_gpu_general import compare, oracle_general, run_general
+from tests.test_gpu_general import check_exit_eval, compare, oracle_general, run_exit_eval, run_general
 
 pytestmark = pytest.mark.gpu
 
@@ -81,3 +82,33 @@ def test_random_general_parity(name, ov, extras, flags):
     g = run_general(x, flags)
     ref = oracle_general(x, flags)
     compare(g, ref, x["cfg"].dtype, flags, name)
+
+
+def _eval_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = [256, 1024, 2048, 2560, 72, 24][i % 6]  # 128-, 64-, 48-row tiles, vector-ALU bf16 and fp32
+        K = int(rng.integers(1, 4))
+        T = int(rng.integers(1, 400))  # up to four 128-row tiles, ragged
+        V = int(rng.integers(1, 600))
+        extras = dict(tau=bool(rng.random() < 0.5), bias=bool(rng.random() < 0.5),
+                      per_module_gain=bool(rng.random() < 0.3),
+                      wbar=str(rng.choice(["none", "shared", "per_head"])))
+        if K == 1:
+            extras["wbar"] = "none"  # no heads
+        cfg = "tiny" if d == 24 else ("2b" if d == 2560 else "1b")
+        out.append((f"e{i}_K{K}_T{T}_d{d}_V{V}", cfg, dict(K=K, T=T, d=d, V=V), extras))
+    return out
+
+
+EVAL_CASES = _eval_cases(12, 2027)
+
+
+@pytest.mark.parametrize("name,cfg,ov,extras", EVAL_CASES, ids=[c[0] for c in EVAL_CASES])
+def test_random_exit_eval_parity(name, cfg, ov, extras):
+    seed = zlib.crc32(name.encode()) % 1000
+    x = make_extras(make_inputs(cfg, seed=seed, **ov), seed, **extras)
+    log(f"eval case {name}: extras {extras}")
+    losses, row_loss, top1 = run_exit_eval(x)
+    check_exit_eval(x, losses, row_loss, top1, name, min_rows_for_agreement=50)
