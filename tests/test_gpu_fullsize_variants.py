@@ -42,8 +42,9 @@ def _check_top1(top1_rows, ref, V, dtype, what):
     assert agree >= 0.9
 
 
-@pytest.mark.parametrize("name,extras", [("1b", dict()), ("2b", dict(tau=True, bias=True))],
-                         ids=["1b_plain", "2b_tau_bias"])
+@pytest.mark.parametrize("name,extras", [("1b", dict()), ("2b", dict(tau=True, bias=True)),
+                                         ("340m", dict(tau=True, bias=True))],
+                         ids=["1b_plain", "2b_tau_bias", "340m_tau_bias"])
 def test_fullsize_exit_eval(name, extras):
     import torch
 
@@ -73,12 +74,13 @@ def test_fullsize_exit_eval(name, extras):
     _check_top1(top1[:, rows], ref, cfg.V, cfg.dtype, f"exit eval {name}")
 
 
-def test_fullsize_general_tau_bias():
-    x = make_extras(make_inputs("1b", seed=0), 0, tau=True, bias=True)
+@pytest.mark.parametrize("name", ["1b", "340m"])
+def test_fullsize_general_tau_bias(name):
+    x = make_extras(make_inputs(name, seed=0), 0, tau=True, bias=True)
     cfg = x["cfg"]
     K, T = cfg.K, cfg.T
     flags = dict(final_module_dW=True, want_dtau=True, want_dbias=True)
-    log(f"full-size general call 1b with temperatures and biases: K={K} T={T} d={cfg.d} V={cfg.V}")
+    log(f"full-size general call {name} with temperatures and biases: K={K} T={T} d={cfg.d} V={cfg.V}")
     g = run_general(x, flags)
     for key in ("losses", "row_loss", "dh", "dW", "dgain", "dtau", "dbias"):
         assert np.all(np.isfinite(g[key])), key
