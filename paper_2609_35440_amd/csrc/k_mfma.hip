@@ -97,7 +97,7 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
 
 // MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
 // MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
-// EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
+// EXT (LOCAL and EVAL): the variant with per-chunk biases, launched when the call has biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     constexpr bool PC = MODE == LOCAL || MODE == RGRAD;     // second product
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     constexpr int NR = G::NR;
     constexpr int PR = G::PR;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
-    constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
+    constexpr bool BZ = (MODE == LOCAL || MODE == EVAL) && EXT;  // per-chunk biases through LDS
     // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
     // the logit products, [kDmaA, NI) after the elementwise step.  Measured:
     // with a second product, at d = 2048 5 of 8 inside the products (3 and 8
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         }
         if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
     }
-    const bool has_bias = (MODE == LOCAL && EXT) || a.bias != nullptr;  // the bias variant always has one
+    const bool has_bias = BZ || a.bias != nullptr;  // the bias variant always has one
 
     ChunkStream<DS> stream;
     stream.init(d, js, lane);
@@ -669,7 +669,9 @@ int mfma_rows(int d) { return d <= NW * 128 ? rows_of<128, true>() : rows_of<256
 hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s) {
     return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
 }
-hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s) { return launch_mode<EVAL, true>(a, 0, s); }
+hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s) {
+    return a.bias ? launch_mode<EVAL, true>(a, 0, s) : launch_mode<EVAL, false>(a, 0, s);
+}
 hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s) {
     return launch_mode<RGRAD, false>(a, nmod, s);
 }

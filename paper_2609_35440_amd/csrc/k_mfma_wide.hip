@@ -76,7 +76,7 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
 // MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
 // MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
 // XR = 16 with a second product (LOCAL, RGRAD), 48 without (EVAL, BGRAD).
-// EXT (LOCAL only): the variant with per-chunk biases; EVAL always handles biases.
+// EXT (LOCAL and EVAL): the variant with per-chunk biases, launched when the call has biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;           // X = h, Y = readout
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     constexpr int NXB = XR / 16;                                 // 16-row blocks of the logit product
     static_assert((PC && XR == 16) || (!PC && (XR == 16 || XR == 32 || XR == 48)), "tile height");
     using G = Geo<DS, XR>;
-    constexpr bool BZ = (MODE == LOCAL && EXT) || MODE == EVAL;  // per-chunk biases through LDS
+    constexpr bool BZ = (MODE == LOCAL || MODE == EVAL) && EXT;  // per-chunk biases through LDS
     constexpr int RA = 4;                                        // row-wise reads in flight
     __shared__ __attribute__((aligned(16))) char ybuf[G::YBUF];
     __shared__ __attribute__((aligned(16))) float part[NW * XR * PP];
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         }
         if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
     }
-    const bool has_bias = (MODE == LOCAL && EXT) || a.bias != nullptr;  // the bias variant always has one
+    const bool has_bias = BZ || a.bias != nullptr;  // the bias variant always has one
 
     // ---- staged stream: lane p of load q fetches slot 64 q + p of the wave's
     // slice (row-contiguous), with zeros past the last streamed row
@@ -510,7 +510,9 @@ bool mfma_wide_supported(int dtype, int d) { return dtype == 0 && d == 2560; }
 hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, hipStream_t s) {
     return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
 }
-hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s) { return launch_mode<EVAL, true>(a, 0, s); }
+hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s) {
+    return a.bias ? launch_mode<EVAL, true>(a, 0, s) : launch_mode<EVAL, false>(a, 0, s);
+}
 hipError_t launch_readout_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s) {
     return launch_mode<RGRAD, false>(a, nmod, s);
 }
