@@ -151,19 +151,23 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "he
     }
 
 
-def kernel_sources_hash(read=None) -> str:
-    """Hash of the matrix-core kernel sources, comments and whitespace removed
-    (stamps counter-derived traffic: a comment edit does not void a measurement)."""
+def kernel_sources_hash(read=None, files=None) -> str:
+    """Hash of every library source (paper_2609_35440_amd/csrc), comments and
+    whitespace removed (stamps counter-derived traffic and profiles: a comment
+    edit does not void a measurement)."""
     import hashlib
     import re
 
+    csrc = os.path.join(ROOT, "paper_2609_35440_amd", "csrc")
     if read is None:
         def read(f):
-            with open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f), "rb") as fh:
+            with open(os.path.join(csrc, f), "rb") as fh:
                 return fh.read().decode()
+    if files is None:
+        files = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
 
     h = hashlib.sha256()
-    for f in ("k_mfma.hip", "mfma_common.h", "mfma_layout.h", "solo_internal.h"):
+    for f in files:
         text = re.sub(r"/\*.*?\*/", " ", read(f), flags=re.S)
         text = re.sub(r"//[^\n]*", " ", text)
         h.update(" ".join(text.split()).encode())

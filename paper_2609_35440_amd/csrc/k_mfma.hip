@@ -36,9 +36,19 @@
 // LDS, each wave finishes the elementwise step for XR/8 of the stationary
 // rows, and every wave then accumulates its own column slice of the second
 // product.  The accumulator (XR rows x d/8 columns, fp32) and the stationary
-// operand stay in registers for the whole pass; the streamed chunk goes
-// HBM/L2 -> LDS directly and is read twice from LDS: row-wise for the logit
-// product and with the transposing read for the second product.
+// operand stay in registers for the whole pass.
+//
+// Streaming: in the passes with a second product the chunk goes HBM/L2 ->
+// LDS directly and is read twice from LDS: row-wise for the logit product and
+// with the transposing read for the second product.  The passes without one
+// (exit evaluation, bias gradient) stream the tiled copy of Y (see
+// tiled_elems) straight into the registers that feed the logit product, one
+// contiguous 1 KiB per wave and instruction, and need no LDS for the chunk.
+// (Measured at d = 2048: exit evaluation 9.22 -> 8.09 ms, the heads'
+// bias-gradient pass 7.23 -> 6.46 ms.  With a second product the registers
+// still have to be written to LDS for the transposing read, and those
+// ds_write_b128 cost more than the direct-to-LDS stream and the row-wise
+// reads together: local-loss pass 18.0 -> 20.6 ms.)
 #include "mfma_common.h"
 
 namespace solo {
@@ -71,28 +81,31 @@ constexpr int rows_of() { return (!PC && DS <= 128) ? 128 : ((DS <= 128 || (!PC 
 template <int DS, bool PC>
 struct Geo : layout::Geo<DS> {
     static constexpr int XR = rows_of<DS, PC>();       // stationary rows per workgroup
-    // rows of the partial-logit exchange buffer: 64-row tiles at the widest
-    // slices exchange their logits in two rounds of 32 rows (LDS budget)
-    static constexpr int PR = (XR == 64 && DS > 128) ? 32 : XR;
-    static constexpr int NX = XR / PR;                 // exchange rounds per chunk
+    static constexpr int PR = XR;                      // rows of the partial-logit exchange buffer
     static constexpr int NXB = XR / 16;                // 16-row blocks of the logit product
     static constexpr int NR = XR / 32;                 // 32-row halves of the second product
     // elementwise step: a lane takes EWC adjacent streamed columns of ER
-    // stationary rows, LPR lanes share a row (64-row tiles exchanged in one
-    // round: one row and two columns per lane)
-    static constexpr int EWC = (XR == 64 && NX == 1) ? 2 : 1;
+    // stationary rows, LPR lanes share a row (64-row tiles: one row and two
+    // columns per lane)
+    static constexpr int EWC = XR == 64 ? 2 : 1;
     static constexpr int ER = NR / EWC;
     static constexpr int LPR = 16 / EWC;
     static constexpr int NB = DS / 32;                 // 32-column accumulator blocks per wave
     static constexpr int NK = DS / 32;                 // 32-deep k-steps of the logit product
-    static constexpr int YBUF = NW * layout::Geo<DS>::SLICE;  // one chunk buffer (all waves)
+    // one chunk buffer (all waves); the passes without a second product keep no chunk in LDS
+    static constexpr int YBUF = PC ? NW * layout::Geo<DS>::SLICE : 16;
     static constexpr int GB = PC ? XR * YC : 8;        // elements of the probability tile (second product only)
-    static constexpr int TOTAL = 2 * YBUF + NW * PR * PP * 4 + GB * 2 + 2 * XR * 4 + NW * XR * 4 + 4 * YC * 4;
+    static constexpr int TOTAL = 2 * YBUF + NW * PR * PP * 4 + GB * 2 + 3 * XR * 4 + NW * XR * 4 + 4 * YC * 4;
     static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
 __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
     return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
+}
+
+// the tiled copy of module k's readout (exit evaluation)
+__device__ __forceinline__ const bf16* tiled_readout_of(const FusedArgs& a, int k) {
+    return k == a.K - 1 ? (const bf16*)a.Wtt : (const bf16*)a.Wht + (long long)k * a.wht_stride;
 }
 
 // MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
@@ -106,6 +119,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     constexpr int NR = G::NR;
     constexpr int PR = G::PR;
     constexpr bool LL = MODE == LOCAL || MODE == EVAL;      // X = h, Y = readout
+    constexpr bool RF = !PC;                                // operand registers fed from the tiled copy
     constexpr bool BZ = (MODE == LOCAL || MODE == EVAL) && EXT;  // per-chunk biases through LDS
     // the stream of the next chunk: instructions [0, kDmaA) one per k-step of
     // the logit products, [kDmaA, NI) after the elementwise step.  Measured:
@@ -113,7 +127,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     // are 3-5% slower, 4 and 6 within box-to-box noise), at d = 1024 2 of 4 (3%
     // faster than 3 of 4); without one (64-row tiles, twice the products per
     // chunk) all of them, 12-14% faster than 5 of 8 at d = 2048
-    constexpr int kDmaA = PC ? ((DS <= 128 ? 4 : 5) * G::NI + 7) / 8 : G::NI;
+    constexpr int kDmaA = ((DS <= 128 ? 4 : 5) * G::NI + 7) / 8;
     // Separate LDS objects, so that the compiler can tell the chunk being read
     // from the chunk being prefetched (no needless waits on the prefetch).
     __shared__ __attribute__((aligned(16))) char ybufA[G::YBUF];
@@ -122,6 +136,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     __shared__ __attribute__((aligned(16))) bf16 gbuf[G::GB];
     __shared__ float abuf[XR];
     __shared__ float sbuf[XR];
+    __shared__ float pybuf[XR];
     __shared__ float cbuf[NW * XR];
     // per-chunk side data streamed next to the chunk: the per-token records
     // (readout-/bias-gradient passes) or the chunk's 16 biases (local loss)
@@ -141,7 +156,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const bf16* __restrict__ Rk = readout_of(a, k);
     const bf16* __restrict__ gk = (const bf16*)a.gain + (long long)k * a.g_stride;
     const bf16* __restrict__ X = LL ? hk : Rk;
-    const bf16* __restrict__ Y = LL ? Rk : (const bf16*)a.hg + (long long)(k - a.hg_m0) * a.T * d;
+    // the streamed rows: the readout, or the copy of g_k * h_k (row-major for
+    // the direct-to-LDS stream, tiled for the register-fed passes); module
+    // copies sit tiled_elems(T, d) apart either way
+    const bf16* __restrict__ Y = LL ? (RF ? tiled_readout_of(a, k) : Rk)
+                                    : (const bf16*)a.hg + (long long)(k - a.hg_m0) * tiled_elems(a.T, d);
     const int nX = LL ? a.T : a.V;
     const int nY = LL ? a.V : a.T;
     const int nchunks = (nY + YC - 1) / YC;
@@ -159,30 +178,51 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int yy = EWC == 2 ? 2 * (lane & 7) : (lane & 15);
     const int lane16 = lane & 15;  // the 16 lanes that stream a chunk's side data
     float own_r2[ER];  // LL: r_t tau_k log2 e of row xo (r_t is read again after the loop)
-    int own_tgt[ER];   // LL: target of row xo
+    // LL: target of row xo minus yy, the chunk start y0 at which this lane meets
+    // it (the target itself is read again after the loop)
+    int tgt_rel[ER];
     float bx2[ER];     // readout-/bias-gradient passes: bias of the stationary readout row, base 2
 #pragma unroll
     for (int r = 0; r < ER; ++r) {
         own_r2[r] = 0.f;
-        own_tgt[r] = -1;
+        tgt_rel[r] = -1 - yy;
         bx2[r] = 0.f;
         if (LL && x0 + xo[r] < nX) {
             own_r2[r] = a.rstd[modoff + x0 + xo[r]] * tau_k * kLog2e;
-            own_tgt[r] = a.targets[modoff + x0 + xo[r]];
+            tgt_rel[r] = a.targets[modoff + x0 + xo[r]] - yy;
         }
         if (!LL && a.bias && x0 + xo[r] < nX) bx2[r] = a.bias[(long long)k * a.V + x0 + xo[r]] * kLog2e;
     }
     const bool has_bias = BZ || a.bias != nullptr;  // the bias variant always has one
 
     ChunkStream<DS> stream;
-    stream.init(d, js, lane);
+    if (PC) stream.init(d, js, lane);
     // first chunk in flight before the stationary operand is read
     const unsigned sliceA_u = lds_addr(sliceA), sliceB_u = lds_addr(sliceB);
-    stream.issue(Y, nY, d, 0, sliceA_u);
+    if (PC) stream.issue(Y, nY, d, 0, sliceA_u);
+    // register-fed passes: k-step kk of chunk c of this wave's slice is NK KiB
+    // into chunk c of the tiled copy plus 1 KiB kk; buffer loads over those NK
+    // KiB, one lane offset shared by every load and the k-step as a scalar offset
+    const bf16* __restrict__ Yw = Y + w * (G::NK * 512);
+    auto rsrc_of = [&](int c) __attribute__((always_inline)) {
+        return __builtin_amdgcn_make_buffer_rsrc((void*)(Yw + (long long)c * 16 * d), (short)0, G::NK * 1024,
+                                                 0x00020000);
+    };
+    auto ld_op = [&](__amdgpu_buffer_rsrc_t rs, int kk) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, kk * 1024, 0));
+    };
+    // operand registers of the register-fed passes: k-step kk of the current
+    // chunk (lane: streamed row lane % 16, columns js + 32 kk + 8 (lane / 16) .. + 7)
+    bf16x8 ay_rf[RF ? G::NK : 1];
+    if (RF) {
+#pragma unroll
+        for (int kk = 0; kk < G::NK; ++kk) ay_rf[kk] = ld_op(rsrc_of(0), kk);
+    }
     const unsigned recA_u = lds_addr((LDS_AS char*)(LDS_AS void*)recA);
     const unsigned recB_u = lds_addr((LDS_AS char*)(LDS_AS void*)recB);
     auto issue_side = [&](int y0, unsigned dst) __attribute__((always_inline)) {
-        const int rows = nY - y0;
+        // rows of this chunk only (a range over all remaining rows could pass 2^32 bytes)
+        const int rows = nY - y0 < YC ? nY - y0 : YC;
         if (!LL && w == 0 && lane < YC) {
             // the 16 per-token records of the chunk
             const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
@@ -255,60 +295,58 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         const int y0 = c * YC;
         const bool more = c + 1 < nchunks;
         const i32x4 nrs = ChunkStream<DS>::rsrc(Y, nY, d, y0 + YC);
+        // register-fed passes reload the operand registers with the next chunk
+        // (the last chunk reloads itself: no branch around the loads)
+        const __amdgpu_buffer_rsrc_t yn = rsrc_of(more ? c + 1 : c);
 
         // ---- split-K partial of the logit tile S[y][x] over this wave's columns.
         // All operand reads go out first, ahead of the data of the next chunk,
-        // whose stream is spread over the products (and, in the passes with a
-        // second product, the end of the elementwise step), so that neither the
-        // texture unit's queue nor the LDS write port sees the whole chunk at once.
-        bf16x8 ay[G::NK];
+        // whose stream is spread over the products (and the end of the
+        // elementwise step), so that neither the texture unit's queue nor the
+        // LDS write port sees the whole chunk at once.
+        bf16x8 ay[PC ? G::NK : 1];
+        if (PC) {
+            // the widest slices recompute the per-lane part of the row-wise read
+            // address each step (no register left to hold it)
+            const int ao = DS >= 224 ? layout::rowread_off<DS>(lane_now()) : a_off;
 #pragma unroll
-        for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + a_off + 64 * kk);
+            for (int kk = 0; kk < G::NK; ++kk) ay[kk] = *(LDS_AS bf16x8*)(cur + ao + 64 * kk);
+        }
         if (more) issue_side(y0 + YC, side_nxt);
         f32x4 S[G::NXB];
 #pragma unroll
         for (int xb = 0; xb < G::NXB; ++xb) S[xb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
+            if constexpr (RF) {
 #pragma unroll
-            for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay[kk], xr[xb][kk], S[xb]);
-            if (kk < kDmaA) {
-                if (more) stream.issue_one(nrs, d, nxt, kk);
-                __builtin_amdgcn_sched_barrier(0);  // keeps the instruction between these products
+                for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay_rf[kk], xr[xb][kk], S[xb]);
+                ay_rf[kk] = ld_op(yn, kk);
+                __builtin_amdgcn_sched_barrier(0);  // keeps the reload behind this k-step's products
+            } else {
+#pragma unroll
+                for (int xb = 0; xb < G::NXB; ++xb) S[xb] = mfma16(ay[kk], xr[xb][kk], S[xb]);
+                if (kk < kDmaA) {
+                    if (more) stream.issue_one(nrs, d, nxt, kk);
+                    __builtin_amdgcn_sched_barrier(0);  // keeps the instruction between these products
+                }
             }
         }
-        const int yg = y0 + yy;
-        // Passes without a second product at two exchange rounds: the second
-        // round's partials go into this wave's own slice of the current chunk,
-        // which no other wave reads and whose row-wise reads have returned
-        // (LDS operations of a wave run in order); the chunk buffer is next
-        // written by the stream of the chunk after next, behind this step's
-        // last barrier.  Both rounds then meet behind one barrier.
-        constexpr bool FOLD = !PC && G::NX == 2;
-        static_assert(!FOLD || PR * PP * 4 <= G::SLICE, "a round of partials fits a wave's chunk slice");
-        LDS_AS float* const slices0 = (LDS_AS float*)(LDS_AS void*)(cur - w * G::SLICE);
+        const int ylim = nY - y0;  // columns yy >= ylim of this chunk are past the last streamed row
+        // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
-        for (int rr = 0; rr < G::NX; ++rr) {
-            // exchange round rr: the partials of stationary rows [rr PR, (rr + 1) PR)
-            if (!FOLD || rr == 0) {
-                if (rr > 0) lds_barrier();  // every wave has read the previous round's partials
-                // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
-#pragma unroll
-                for (int xb = rr * (G::NXB / G::NX); xb < (FOLD ? G::NXB : (rr + 1) * (G::NXB / G::NX)); ++xb) {
-                    const int ro = FOLD ? xb / (G::NXB / G::NX) : rr;  // the round of this block
-                    const int xl = 16 * xb - PR * ro + (lane & 15);
-                    LDS_AS float* dst = (FOLD && ro == 1) ? slices0 + w * (G::SLICE / 4)
-                                                          : (LDS_AS float*)(LDS_AS void*)part + w * PR * PP;
-                    *(LDS_AS f32x4*)(dst + xl * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) = S[xb];
-                }
-                lds_barrier();
-            }
-
+        for (int xb = 0; xb < G::NXB; ++xb) {
+            const int xl = 16 * xb + (lane & 15);
+            *(LDS_AS f32x4*)((LDS_AS float*)(LDS_AS void*)part + (w * PR + xl) * PP + 4 * ((lane >> 4) ^ ((xl >> 1) & 3))) =
+                S[xb];
+        }
+        lds_barrier();
+        {
             // ---- elementwise step for rows xo[r] (lane: row xo[r], columns yy .. yy + EWC - 1)
 #pragma unroll
-            for (int r = rr * (ER / G::NX); r < (rr + 1) * (ER / G::NX); ++r) {
+            for (int r = 0; r < ER; ++r) {
                 float q[EWC][NW];
-                const int xl = xo[r] - PR * rr;
+                const int xl = xo[r];
                 const int yq = yy ^ (4 * ((xl >> 1) & 3));  // (yy even for two columns: both in one group)
 #pragma unroll
                 for (int ww = 0; ww < NW; ++ww) {
@@ -317,8 +355,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                         q[0][ww] = v[0];
                         q[EWC - 1][ww] = v[1];
                     } else {
-                        q[0][ww] = (FOLD && rr == 1) ? slices0[ww * (G::SLICE / 4) + xl * PP + yq]
-                                                     : ((LDS_AS float*)(LDS_AS void*)part)[(ww * PR + xl) * PP + yq];
+                        q[0][ww] = ((LDS_AS float*)(LDS_AS void*)part)[(ww * PR + xl) * PP + yq];
                     }
                 }
                 static_assert(NW == 8, "partial-sum tree");
@@ -335,7 +372,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                     float zmax = -INFINITY;
 #pragma unroll
                     for (int e = 0; e < EWC; ++e) {
-                        float ymask = (yg + e < nY) ? 0.f : -INFINITY;
+                        float ymask = (yy + e < ylim) ? 0.f : -INFINITY;
                         if (BZ && has_bias) ymask += side[yy + e] * kLog2e;
                         zc[e] = __builtin_fmaf(sxy[e], own_r2[r], ymask);
                         zmax = fmaxf(zmax, zc[e]);
@@ -352,26 +389,30 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                     for (int e = 0; e < EWC; ++e) {
                         const float p = __builtin_amdgcn_exp2f(zc[e] - m_run[r]);
-                        s_part[r] += p;
-                        if (yg + e == own_tgt[r]) zy_part[r] = zc[e];
+                        const bool is_y = tgt_rel[r] - e == y0;
+                        s_part[r] += is_y ? 0.f : p;  // the target's term joins at the end (finish_row)
+                        if (is_y) zy_part[r] = zc[e];
                         if (MODE == EVAL && zc[e] > best[r]) {  // strict: the first (lowest) column keeps a tie
                             best[r] = zc[e];
-                            best_v[r] = yg + e;
+                            best_v[r] = y0 + yy + e;
                         }
-                        gval[e] = p;
+                        // the target's probability enters the input gradient in
+                        // the epilogue, in fp32 together with its one-hot term
+                        gval[e] = is_y ? 0.f : p;
                     }
                     if (MODE == LOCAL) abuf[xo[r]] = alpha;  // the lanes of a row store the same value
                 } else {
 #pragma unroll
                     for (int e = 0; e < EWC; ++e) {
-                        // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
-                        // the end of the module read as zeros and are masked
+                        // record {lse log2 e, r tau log2 e, target, p_y - 1}; tokens past
+                        // the end of the module read as zeros and are masked.  The
+                        // target's entry of delta is the exact p_y - 1 of the local-loss pass.
                         const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * (yy + e));
                         const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy[e], r4[1], bx2[r] - r4[0]));
                         // (a padded token's zero record would match readout row 0 as its target)
                         const float dlt =
-                            (yg + e < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
-                        gval[e] = dlt * r4[3];
+                            (yy + e < ylim) ? (__float_as_int(r4[2]) == x0 + xo[r] ? r4[3] : p) : 0.f;
+                        gval[e] = dlt * (r4[1] * (kLn2 * a.inv_T));  // times r tau / T
                         db_part[r] += dlt;
                     }
                 }
@@ -388,7 +429,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
                 }
             }
         }
-        if (more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
+        if (PC && more) stream.template issue_range<kDmaA, G::NI>(nrs, d, nxt);
         lds_barrier();
 
         // 64-row tiles: the second product runs at raised wave priority, so that
@@ -451,7 +492,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // finish the online softmax of rows xo[r]
 #pragma unroll
         for (int r = 0; r < ER; ++r) {
-            const float s = group_sum<LPR>(s_part[r]);
+            const int own_tgt = x0 + xo[r] < nX ? a.targets[modoff + x0 + xo[r]] : -1;
+            const float sx = group_sum<LPR>(s_part[r]);
             const float zy = group_sum<LPR>(zy_part[r]);
             float bst = best[r];
             int bv = best_v[r];
@@ -469,21 +511,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             }
             if (lane % LPR == 0) {
                 const int xr_ = x0 + xo[r];
-                const float r_row = (xr_ < nX) ? a.rstd[modoff + xr_] : 0.f;
-                const float lse2 = m_run[r] + __log2f(s);
-                const bool tok = own_tgt[r] >= 0 && own_tgt[r] < nY;
-                const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
+                const bool tok = own_tgt >= 0 && own_tgt < nY;
+                const RowEnd re = finish_row(m_run[r], sx, zy, tok);
                 if (xr_ < nX) {
                     const long long t = modoff + xr_;
-                    a.lse[t] = lse2 * kLn2;
-                    a.rowloss[t] = rl;
+                    a.lse[t] = re.lse2 * kLn2;
+                    a.rowloss[t] = re.loss;
                     if (MODE == EVAL && a.top1) a.top1[t] = bv;
                     if (MODE == LOCAL && a.rowrec) {
-                        f32x4 rec4 = {lse2, own_r2[r], __int_as_float(own_tgt[r]), r_row * tau_k * a.inv_T};
+                        f32x4 rec4 = {re.lse2, own_r2[r], __int_as_float(own_tgt), re.py1};
                         *(f32x4*)(a.rowrec + 4 * t) = rec4;
                     }
                 }
-                sbuf[xo[r]] = 1.f / s;
+                sbuf[xo[r]] = re.inv_s;
+                // p_y - 1: the target's probability was left out of the probability tile
+                if (MODE == LOCAL) pybuf[xo[r]] = re.py1;
             }
         }
     }
@@ -495,10 +537,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         bool xok[NR], tok[NR];
         float rx[NR];
         const bf16* hrow[NR];
-        // sweep 1: acc <- e = (acc / s - R_y) / T, so that dhhat = tau e, and the
-        // row sums of e * g * n (n = r h).  That row sum is both the RMSNorm
-        // backward's mean(dn * n) = tau sum / d and the token's share of
-        // d loss / d tau = sum_v delta_v u_v = <sum_v delta_v R_v, g * n>.
+        // sweep 1: acc <- e = (acc / s + (p_y - 1) R_y) / T, so that dhhat = tau e
+        // (acc holds every column but the target's, whose probability term
+        // joins its one-hot term here in fp32), and the row sums of e * g * n
+        // (n = r h).  That row sum is both the RMSNorm backward's mean(dn * n)
+        // = tau sum / d and the token's share of d loss / d tau = sum_v
+        // delta_v u_v = <sum_v delta_v R_v, g * n>.
 #pragma unroll
         for (int h = 0; h < NR; ++h) {
             const int xg = x0 + 32 * h + ex;
@@ -507,6 +551,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const int tgt = xok[h] ? a.targets[modoff + xg] : -1;
             tok[h] = tgt >= 0 && tgt < nY;
             const float inv_s = sbuf[32 * h + ex];
+            const float py1 = pybuf[32 * h + ex];
             hrow[h] = hk + (long long)(xok[h] ? xg : 0) * d;
             const bf16* wrow = Rk + (long long)(tok[h] ? tgt : 0) * d;
             float cp = 0.f;
@@ -523,7 +568,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float wy = tok[h] ? bf16_bits_to_f32(wv[e]) : 0.f;
-                        const float ev = (acc[b][h][4 * i4 + e] * inv_s - wy) * a.inv_T;
+                        const float ev = __builtin_fmaf(acc[b][h][4 * i4 + e], inv_s, py1 * wy) * a.inv_T;
                         cp += bf16_bits_to_f32(gv[e]) * ev * (rx[h] * bf16_bits_to_f32(hv[e]));
                         acc[b][h][4 * i4 + e] = ev;
                     }

@@ -14,17 +14,16 @@
 //   - the second product runs on the 16x16x16 instruction (its contraction
 //     over the 16 streamed rows of a chunk), its streamed operand read with
 //     one ds_read_b64_tr_b16 per product;
-//   - one chunk is 16 x d bf16 = 80 KiB at d = 2560, so two of them do not
-//     fit next to the partial-logit exchange in 160 KiB of LDS.  The chunk
-//     lives in one LDS buffer, and the next one is staged through registers:
-//     row-contiguous global loads are issued a whole chunk ahead, and written
-//     to LDS once the current chunk's last read has returned.
+//   - the streamed rows come from their tiled copy (see tiled_elems): each
+//     wave loads its 10 k-steps of a chunk, one contiguous 1 KiB per
+//     instruction, straight into the registers that feed the logit product.
 //
-// Per chunk each wave (1) reads its slice row-wise and computes its split-K
-// partial of the 16 x XR logit tile; (2) the 8 partials meet in LDS and each
-// wave finishes the elementwise step for XR / 8 of the stationary rows;
-// (3) every wave accumulates its column slice of the second product; then
-// (4) it writes the staged next chunk into its slice and stages the one after.
+// Per chunk each wave (1) computes its split-K partial of the 16 x XR logit
+// tile from its operand registers, writes them into its private LDS slice
+// (passes with a second product) and reloads them with the next chunk;
+// (2) the 8 partials meet in LDS and each wave finishes the elementwise step
+// for XR / 8 of the stationary rows; (3) every wave accumulates its column
+// slice of the second product, reading its slice back transposed.
 #include "mfma_common.h"
 #include "mfma_layout_wide.h"
 
@@ -86,12 +85,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     static_assert((PC && XR == 16) || (!PC && (XR == 16 || XR == 32 || XR == 48)), "tile height");
     using G = Geo<DS, XR>;
     constexpr bool BZ = (MODE == LOCAL || MODE == EVAL) && EXT;  // per-chunk biases through LDS
-    constexpr int RA = 4;                                        // row-wise reads in flight
-    __shared__ __attribute__((aligned(16))) char ybuf[G::YBUF];
+    __shared__ __attribute__((aligned(16))) char ybuf[PC ? G::YBUF : 16];
     __shared__ __attribute__((aligned(16))) float part[NW * XR * PP];
     __shared__ __attribute__((aligned(16))) bf16 gbuf[XR * YC];
     __shared__ float abuf[XR];
     __shared__ float sbuf[XR];
+    __shared__ float pybuf[XR];
     __shared__ float cbuf[NW * XR];
     __shared__ __attribute__((aligned(16))) float recA[YC * 4];
     __shared__ __attribute__((aligned(16))) float recB[YC * 4];
@@ -109,10 +108,29 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     const bf16* __restrict__ Rk = readout_of(a, k);
     const bf16* __restrict__ gk = (const bf16*)a.gain + (long long)k * a.g_stride;
     const bf16* __restrict__ X = LL ? hk : Rk;
-    const bf16* __restrict__ Y = LL ? Rk : (const bf16*)a.hg + (long long)(k - a.hg_m0) * a.T * d;
     const int nX = LL ? a.T : a.V;
     const int nY = LL ? a.V : a.T;
     const int nchunks = (nY + YC - 1) / YC;
+    // this wave's k-step 0 of chunk 0 in the tiled streamed operand; k-step kk
+    // of chunk c is 512 kk + 16 d c elements further, the lane's 16 bytes 8 lane
+    const bf16* __restrict__ Yw =
+        (LL ? (k == a.K - 1 ? (const bf16*)a.Wtt : (const bf16*)a.Wht + (long long)k * a.wht_stride)
+            : (const bf16*)a.hg + (long long)(k - a.hg_m0) * tiled_elems(a.T, d)) +
+        w * (G::NK * 512);
+    const long long cstride = 16LL * d;
+    // buffer loads over this wave's NK KiB of a chunk, one lane offset shared by
+    // every load and the k-step as a scalar offset
+    auto rsrc_of = [&](const bf16* __restrict__ base) __attribute__((always_inline)) {
+        return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, G::NK * 1024, 0x00020000);
+    };
+    auto ld_op = [&](__amdgpu_buffer_rsrc_t rs, int kk) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rs, lane * 16, kk * 1024, 0));
+    };
+    // operand registers: k-step kk of the current chunk (lane: streamed row
+    // lane % 16, columns js + 32 kk + 8 (lane / 16) .. + 7)
+    bf16x8 ay[G::NK];
+#pragma unroll
+    for (int kk = 0; kk < G::NK; ++kk) ay[kk] = ld_op(rsrc_of(Yw), kk);
 
     LDS_AS char* slice = (LDS_AS char*)(LDS_AS void*)ybuf + w * G::SLICE;
 
@@ -147,29 +165,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     }
     const bool has_bias = BZ || a.bias != nullptr;  // the bias variant always has one
 
-    // ---- staged stream: lane p of load q fetches slot 64 q + p of the wave's
-    // slice (row-contiguous), with zeros past the last streamed row
-    i32x4 stg[G::NI];
-    auto stage_load = [&](int y0) __attribute__((always_inline)) {
-        const int rows = nY - y0 < YC ? nY - y0 : YC;
-        const int rem = rows > 0 ? rows * d * 2 - 2 * js : 0;  // rows of this chunk only
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(Y + (long long)(rows > 0 ? y0 : 0) * d + js), (short)0, rem > 0 ? rem : 0, 0x00020000);
-#pragma unroll
-        for (int q = 0; q < G::NI; ++q) {
-            const int off = (layoutw::stage_row<DS>(q, lane) * d + 8 * layoutw::stage_gran<DS>(q, lane)) * 2;
-            stg[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
-        }
-    };
-    auto stage_store = [&]() __attribute__((always_inline)) {
-#pragma unroll
-        for (int q = 0; q < G::NI; ++q) *(LDS_AS i32x4*)(slice + layoutw::stage_dst<DS>(q, lane)) = stg[q];
-    };
-
     const unsigned recA_u = lds_addr((LDS_AS char*)(LDS_AS void*)recA);
     const unsigned recB_u = lds_addr((LDS_AS char*)(LDS_AS void*)recB);
     auto issue_side = [&](int y0, unsigned dst) __attribute__((always_inline)) {
-        const int rows = nY - y0;
+        // rows of this chunk only (a range over all remaining rows could pass 2^32 bytes)
+        const int rows = nY - y0 < YC ? nY - y0 : YC;
         if (!LL && w == 0 && lane < YC) {
             // the 16 per-token records of the chunk
             const unsigned rem = rows > 0 ? (unsigned)rows * 16u : 0u;
@@ -182,12 +182,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         }
     };
 
-    // first chunk: side data, staged load, then its LDS write; the second chunk staged
     issue_side(0, recA_u);
-    stage_load(0);
-    wait_vm();
-    stage_store();
-    if (nchunks > 1) stage_load(YC);
 
     // stationary operand (local loss and exit evaluation: times the gain,
     // rounded once): B of the 16x16x32 logit product, lane holds
@@ -233,7 +228,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         best_v[r] = -1;
     }
 
-    // row-wise read of k-step kk at rd_even + 64 kk (kk even) or rd_odd + 64 kk (kk odd):
+    // the operand registers of k-step kk go where the row-wise read of the slice
+    // layout finds them: rd_even + 64 kk (kk even) or rd_odd + 64 kk (kk odd);
     // the swizzle flips bit 2 of the granule index for rows with (r & 4)
     const int rd_even = layoutw::rowread_off<DS>(lane, 0);
     const int rd_odd = layoutw::rowread_off<DS>(lane, 1) - 64;
@@ -241,23 +237,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     auto step = [&](LDS_AS float* side, unsigned side_nxt, int c) __attribute__((always_inline)) {
         const int y0 = c * YC;
         const bool more = c + 1 < nchunks;
+        // reload with the next chunk (the last chunk reloads itself, unused)
+        const __amdgpu_buffer_rsrc_t yn = rsrc_of(Yw + (more ? (long long)(c + 1) : (long long)c) * cstride);
 
         // ---- (1) split-K partial of the logit tile S[y][x] over this wave's columns
-        bf16x8 ay[RA];
-#pragma unroll
-        for (int kk = 0; kk < RA && kk < G::NK; ++kk)
-            ay[kk] = *(LDS_AS bf16x8*)(slice + ((kk & 1) ? rd_odd : rd_even) + 64 * kk);
         if (more) issue_side(y0 + YC, side_nxt);
         f32x4 S[NXB];
 #pragma unroll
         for (int xb = 0; xb < NXB; ++xb) S[xb] = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kk = 0; kk < G::NK; ++kk) {
-            const bf16x8 wa = ay[kk % RA];
-            if (kk + RA < G::NK)
-                ay[kk % RA] = *(LDS_AS bf16x8*)(slice + (((kk + RA) & 1) ? rd_odd : rd_even) + 64 * (kk + RA));
 #pragma unroll
-            for (int xb = 0; xb < NXB; ++xb) S[xb] = mfma16(wa, xr[xb][kk], S[xb]);
+            for (int xb = 0; xb < NXB; ++xb) S[xb] = mfma16(ay[kk], xr[xb][kk], S[xb]);
+            if (PC) *(LDS_AS bf16x8*)(slice + ((kk & 1) ? rd_odd : rd_even) + 64 * kk) = ay[kk];
+            ay[kk] = ld_op(yn, kk);
+            __builtin_amdgcn_sched_barrier(0);  // keeps the reload behind this k-step's uses
         }
         // C layout: lane holds S[y = 4 (lane/16) + i][x = 16 xb + lane%16]; store as part[w][x][y]
 #pragma unroll
@@ -292,22 +286,25 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
                     }
                 }
                 const float p = __builtin_amdgcn_exp2f(zc - m_run[r]);
-                s_part[r] += p;
+                s_part[r] += yg == own_tgt[r] ? 0.f : p;  // the target's term joins at the end (finish_row)
                 if (yg == own_tgt[r]) zy_part[r] = zc;
                 if (MODE == EVAL && zc > best[r]) {  // strict: the first (lowest) column keeps a tie
                     best[r] = zc;
                     best_v[r] = yg;
                 }
-                gval = p;
+                // the target's probability enters the input gradient in the
+                // epilogue, in fp32 together with its one-hot term
+                gval = yg == own_tgt[r] ? 0.f : p;
                 if (MODE == LOCAL && wr[r]) abuf[xo[r]] = alpha;  // the 16 lanes of a row store the same value
             } else {
-                // record {lse log2 e, r tau log2 e, target, r tau / T}; tokens past
-                // the end of the module read as zeros and are masked
+                // record {lse log2 e, r tau log2 e, target, p_y - 1}; tokens past
+                // the end of the module read as zeros and are masked.  The target's
+                // entry of delta is the exact p_y - 1 of the local-loss pass.
                 const f32x4 r4 = *(LDS_AS f32x4*)(side + 4 * yy);
                 const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sxy, r4[1], bx2[r] - r4[0]));
                 // (a padded token's zero record would match readout row 0 as its target)
-                const float dlt = (yg < nY) ? p - (__float_as_int(r4[2]) == x0 + xo[r] ? 1.f : 0.f) : 0.f;
-                gval = dlt * r4[3];
+                const float dlt = (yg < nY) ? (__float_as_int(r4[2]) == x0 + xo[r] ? r4[3] : p) : 0.f;
+                gval = dlt * (r4[1] * (kLn2 * a.inv_T));  // times r tau / T
                 db_part[r] += dlt;
             }
             if (PC && wr[r]) gbuf[xo[r] * YC + (yy ^ (8 * ((xo[r] >> 3) & 1)))] = (bf16)gval;
@@ -333,16 +330,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
                 acc[PC ? b : 0] = mfma16k16(t, gfrag, acc[PC ? b : 0]);
             }
         }
-        // ---- (4) the next chunk into the slice once this chunk's reads have returned
-        // (LDS operations of a wave run in order); its side data and staged
-        // loads have landed after the vmcnt wait; then stage the chunk after it
+        // the next chunk's operand registers and side data have arrived; the
+        // slice is rewritten by the next logit product only after this
+        // chunk's transposing reads (LDS operations of a wave run in order)
+        __builtin_amdgcn_sched_barrier(0);
         wait_vm();
-        if (more) {
-            stage_store();
-            __builtin_amdgcn_sched_barrier(0);
-            if (c + 2 < nchunks) stage_load(y0 + 2 * YC);
-        }
     };
+
+    wait_vm();
 
     for (int c = 0; c < nchunks; c += 2) {
         step((LDS_AS float*)(LDS_AS void*)recA, recB_u, c);
@@ -356,7 +351,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         // finish the online softmax of rows xo[r]
 #pragma unroll
         for (int r = 0; r < ER; ++r) {
-            const float s = row16_sum(s_part[r]);
+            const float sx = row16_sum(s_part[r]);
             const float zy = row16_sum(zy_part[r]);
             float bst = best[r];
             int bv = best_v[r];
@@ -374,21 +369,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
             }
             if (yy == 0 && wr[r]) {
                 const int xr_ = x0 + xo[r];
-                const float r_row = (xr_ < nX) ? a.rstd[modoff + xr_] : 0.f;
-                const float lse2 = m_run[r] + __log2f(s);
                 const bool tok = own_tgt[r] >= 0 && own_tgt[r] < nY;
-                const float rl = tok ? (lse2 - zy) * kLn2 : __int_as_float(0x7fc00000);
+                const RowEnd re = finish_row(m_run[r], sx, zy, tok);
                 if (xr_ < nX) {
                     const long long t = modoff + xr_;
-                    a.lse[t] = lse2 * kLn2;
-                    a.rowloss[t] = rl;
+                    a.lse[t] = re.lse2 * kLn2;
+                    a.rowloss[t] = re.loss;
                     if (MODE == EVAL && a.top1) a.top1[t] = bv;
                     if (MODE == LOCAL && a.rowrec) {
-                        f32x4 rec4 = {lse2, own_r2[r], __int_as_float(own_tgt[r]), r_row * tau_k * a.inv_T};
+                        f32x4 rec4 = {re.lse2, own_r2[r], __int_as_float(own_tgt[r]), re.py1};
                         *(f32x4*)(a.rowrec + 4 * t) = rec4;
                     }
                 }
-                sbuf[xo[r]] = 1.f / s;
+                sbuf[xo[r]] = re.inv_s;
+                // p_y - 1: the target's probability was left out of the probability tile
+                if (MODE == LOCAL) pybuf[xo[r]] = re.py1;
             }
         }
     }
@@ -400,15 +395,17 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         const int tgt = xok ? a.targets[modoff + xg] : -1;
         const bool tok = tgt >= 0 && tgt < nY;
         const float inv_s = sbuf[ex];
+        const float py1 = pybuf[ex];
 
         const bf16* hrow = hk + (long long)(xok ? xg : 0) * d;
         const bf16* wrow = Rk + (long long)(tok ? tgt : 0) * d;
         const bool want_dg = a.dg_mode == 2 || (a.dg_mode == 1 && k == a.K - 1);
         float* dgp = want_dg ? a.dgain_part + ((long long)(a.dg_mode == 2 ? k : 0) * gridDim.x + blockIdx.x) * d
                              : nullptr;
-        // sweep 1: acc <- e = (acc / s - R_y) / T, so that dhhat = tau e, and the
-        // row sums of e * g * n (n = r h): the RMSNorm backward's mean(dn * n) =
-        // tau sum / d and the token's share of d loss / d tau
+        // sweep 1: acc <- e = (acc / s + (p_y - 1) R_y) / T, so that dhhat = tau e
+        // (the target's probability term joins its one-hot term in fp32), and
+        // the row sums of e * g * n (n = r h): the RMSNorm backward's
+        // mean(dn * n) = tau sum / d and the token's share of d loss / d tau
         float cp = 0.f;
 #pragma unroll
         for (int b = 0; b < G::NB; ++b) {
@@ -419,7 +416,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const float wy = tok ? bf16_bits_to_f32(wv[e]) : 0.f;
-                const float ev = (acc[b][e] * inv_s - wy) * a.inv_T;
+                const float ev = __builtin_fmaf(acc[b][e], inv_s, py1 * wy) * a.inv_T;
                 cp += bf16_bits_to_f32(gv[e]) * ev * (rx * bf16_bits_to_f32(hv[e]));
                 acc[b][e] = ev;
             }

@@ -1,8 +1,11 @@
 // Bandwidth-light kernels around the fused passes:
 //   - per-row inverse RMS of the hidden states,
-//   - the gain-scaled copy bf16(g_k * h_k) streamed by the matrix-core gradient passes,
+//   - the copies the matrix-core passes stream: tiled readouts, and the
+//     gain-scaled bf16(g_k * h_k) of the gradient passes (tiled, or row-major
+//     for the direct-to-LDS readout-gradient pass),
 //   - fixed-order reductions for the module losses, the temperature gradients
 //     and the gain gradients.
+#include "mfma_layout.h"
 #include "solo_internal.h"
 
 namespace solo {
@@ -38,16 +41,46 @@ __global__ void k_row_rstd(const E* __restrict__ h, float* __restrict__ rstd, lo
     }
 }
 
-// hg = bf16(h * g) elementwise, 8 elements per thread (d % 8 == 0): the same
-// product and rounding as the stationary-tile load of the local-loss pass.
-__global__ void k_prep_hg(const bf16* __restrict__ h, const bf16* __restrict__ gain, int g_stride,
-                          bf16* __restrict__ hg, int m0, long long per_mod, int T, int d) {
+// Tiled copy of nmat row-major matrices (the streamed-operand layout of the
+// matrix-core passes, see tiled_elems and layout::tile_row / tile_col):
+// thread o of chunk c writes output granule o (zeros past the last row).  With a
+// gain, the copy is bf16(y * g): the same product and rounding as the
+// stationary-tile load of the local-loss pass.
+__global__ void k_tile(const bf16* __restrict__ src, long long src_stride, const bf16* __restrict__ gain,
+                       int g_stride, bf16* __restrict__ dst, int nY, int d) {
+    typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+    const int c = blockIdx.x;
+    const int m = blockIdx.z;
+    const int o = blockIdx.y * blockDim.x + threadIdx.x;
+    if (o >= 2 * d) return;  // 2 d granules of 16 bytes per chunk
+    const int row = 16 * c + layout::tile_row(o);
+    const int j = layout::tile_col(o);
+    bf16x8 v;
+    if (row < nY) {
+        v = *(const bf16x8*)(src + (long long)m * src_stride + (long long)row * d + j);
+        if (gain) {
+            const bf16x8 g = *(const bf16x8*)(gain + (long long)m * g_stride + j);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = (bf16)((float)v[e] * (float)g[e]);
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = (bf16)0.f;
+    }
+    *(bf16x8*)(dst + (long long)m * tiled_elems(nY, d) + (long long)c * 16 * d + 8LL * o) = v;
+}
+
+// Row-major gain-scaled copies hg[m][t][j] = bf16(h[m][t][j] g[m g_stride + j])
+// (the stream of the direct-to-LDS readout-gradient pass), matrices dst_stride
+// elements apart; 8 elements per thread (d % 8 == 0).
+__global__ void k_gain_rows(const bf16* __restrict__ h, long long src_stride, const bf16* __restrict__ gain,
+                            int g_stride, bf16* __restrict__ hg, long long dst_stride, long long per_mod, int d) {
     typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
     const long long n8 = per_mod / 8;
     const int m = blockIdx.y;
-    const bf16* hm = h + (long long)(m0 + m) * per_mod;
-    const bf16* gm = gain + (long long)(m0 + m) * g_stride;
-    bf16* om = hg + (long long)m * per_mod;
+    const bf16* hm = h + (long long)m * src_stride;
+    const bf16* gm = gain + (long long)m * g_stride;
+    bf16* om = hg + (long long)m * dst_stride;
     for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += (long long)gridDim.x * blockDim.x) {
         const int j = (int)((i * 8) % d);
         const bf16x8 hv = *(const bf16x8*)(hm + i * 8);
@@ -109,13 +142,22 @@ hipError_t launch_row_rstd(int dtype, const void* h, float* rstd, long long rows
     return hipGetLastError();
 }
 
-hipError_t launch_prep_hg(const bf16* h, const bf16* gain, int g_stride, bf16* hg, int m0, int nmod, int T, int d,
-                          hipStream_t s) {
+hipError_t launch_tile(const bf16* src, long long src_stride, const bf16* gain, int g_stride, bf16* dst, int nmat,
+                       int nY, int d, hipStream_t s) {
+    const unsigned nchunks = (unsigned)((nY + 15) / 16);
+    const unsigned parts = (unsigned)((2 * d + 255) / 256);
+    hipLaunchKernelGGL(k_tile, dim3(nchunks, parts, (unsigned)nmat), dim3(256), 0, s, src, src_stride, gain, g_stride,
+                       dst, nY, d);
+    return hipGetLastError();
+}
+
+hipError_t launch_gain_rows(const bf16* h, long long src_stride, const bf16* gain, int g_stride, bf16* hg,
+                            long long dst_stride, int nmat, int T, int d, hipStream_t s) {
     const long long per_mod = (long long)T * d;
     long long blocks = (per_mod / 8 + 255) / 256;
     if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(k_prep_hg, dim3((unsigned)blocks, (unsigned)nmod), dim3(256), 0, s, h, gain, g_stride, hg, m0,
-                       per_mod, T, d);
+    hipLaunchKernelGGL(k_gain_rows, dim3((unsigned)blocks, (unsigned)nmat), dim3(256), 0, s, h, src_stride, gain,
+                       g_stride, hg, dst_stride, per_mod, d);
     return hipGetLastError();
 }
 

@@ -40,8 +40,9 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
     float* xs = sm;                    // [RX][d] stationary rows (fp32)
     float* sS = xs + RX * d;           // [RX][YC] logits, then probabilities / deltas
     float* sc = sS + RX * YC;          // [RX] alpha, then 1/s
-    float* sy = sc + RX;               // [3][YC] per-streamed-row scalars (readout-/bias-gradient passes)
-    float* red = sy + 3 * YC;          // [RX][NTHR/64] reductions
+    float* sy = sc + RX;               // [4][YC] per-streamed-row scalars (readout-/bias-gradient passes)
+    float* red = sy + 4 * YC;          // [RX][NTHR/64] reductions
+    float* spy = red + RX * (NTHR / 64);  // [RX] p_y - 1 of the local-loss rows
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -95,6 +96,8 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             sy[tid] = ok ? a.rstd[modoff + yg] : 0.f;
             sy[YC + tid] = ok ? a.lse[modoff + yg] : 0.f;
             sy[2 * YC + tid] = ok ? __int_as_float(a.targets[modoff + yg]) : __int_as_float(-1);
+            // the exact p_y - 1 of the local-loss pass (the target's entry of delta)
+            sy[3 * YC + tid] = ok ? a.rowrec[4 * (modoff + yg) + 3] : 0.f;
         }
         // logits: wave wv handles streamed rows y0 + 16 wv .. +15; lanes split j
         for (int yy = 16 * wv; yy < 16 * wv + 16; ++yy) {
@@ -141,8 +144,10 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             const float m_new = fmaxf(m_run, cmax);
             const float alpha = __expf(m_run - m_new);
             m_run = m_new;
-            const float p0 = (z[0] == -INFINITY) ? 0.f : __expf(z[0] - m_run);
-            const float p1 = (z[1] == -INFINITY) ? 0.f : __expf(z[1] - m_run);
+            // the target's term joins the running sum only at the end of the row,
+            // and its probability the input gradient only in the epilogue
+            const float p0 = (z[0] == -INFINITY || y0 + sq == own_tgt) ? 0.f : __expf(z[0] - m_run);
+            const float p1 = (z[1] == -INFINITY || y0 + sq + 32 == own_tgt) ? 0.f : __expf(z[1] - m_run);
             float ps = p0 + p1;
             for (int off = 16; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 32);
             s_run = s_run * alpha + ps;
@@ -160,7 +165,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                     const float ry = sy[yy];
                     const float p = __expf(tau * ry * sS[sr * YC + yy] + bx - sy[YC + yy]);
                     const int tg = __float_as_int(sy[2 * YC + yy]);
-                    const float dl = p - (tg == xg ? 1.f : 0.f);
+                    const float dl = tg == xg ? sy[3 * YC + yy] : p;
                     dbp += dl;
                     g = dl * ry * tau * a.inv_T;
                 }
@@ -210,15 +215,22 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             }
         }
         if (sq == 0) {
-            const float lse = m_run + logf(s_run);
+            // s_run holds every column but the target's: adding the target's term
+            // here gives p_y - 1 = -s_run / s and the row loss without cancellation
             const bool tok = own_tgt >= 0 && own_tgt < nY;
+            const float ey = tok ? __expf(zy - m_run) : 0.f;
+            const float s = s_run + ey;
+            const float lse = m_run + logf(s);
+            const float py1 = tok ? -s_run / s : 0.f;
             if (x0 + sr < nX) {
                 const long long t = modoff + x0 + sr;
                 a.lse[t] = lse;
-                a.rowloss[t] = tok ? lse - zy : __int_as_float(0x7fc00000);
+                a.rowloss[t] = !tok ? __int_as_float(0x7fc00000) : (ey > s_run ? log1pf(s_run / ey) : (m_run - zy) + logf(s));
                 if (MODE == EVAL && a.top1) a.top1[t] = best_v;
+                if (MODE == LOCAL && a.rowrec) a.rowrec[4 * t + 3] = py1;
             }
-            sc[sr] = 1.f / s_run;
+            sc[sr] = 1.f / s;
+            spy[sr] = py1;
         }
         __syncthreads();
     }
@@ -243,7 +255,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                 const int j = tid + NTHR * q;
                 if (j < d) {
                     const float wy = tok ? ld(Rk, (long long)tg * d + j) : 0.f;
-                    const float ev = (acc[r][q] * sc[r] - wy) * a.inv_T;
+                    const float ev = fmaf(acc[r][q], sc[r], spy[r] * wy) * a.inv_T;
                     const float n = (xg < nX) ? rx * ld(hk, (long long)xg * d + j) : 0.f;
                     const float gj = ld(gk, j);
                     acc[r][q] = tau * gj * ev;          // dn
@@ -307,7 +319,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
 
 template <typename E, int MODE>
 hipError_t launch_t(const FusedArgs& a, int nmod, hipStream_t s) {
-    const size_t lds = sizeof(float) * ((size_t)RX * a.d + RX * YC + RX + 3 * YC + RX * (NTHR / 64));
+    const size_t lds = sizeof(float) * ((size_t)RX * a.d + RX * YC + RX + 4 * YC + RX * (NTHR / 64) + RX);
     hipError_t e = hipFuncSetAttribute((const void*)k_fused_valu<E, MODE>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds);
     if (e != hipSuccess) return e;

@@ -1,6 +1,6 @@
-// Device helpers of the matrix-core passes (k_mfma.hip):
+// Device helpers of the matrix-core passes (k_mfma.hip, k_mfma_wide.hip):
 // operand types, MFMA wrappers, the direct-to-LDS chunk stream, row
-// reductions over 16 lanes and the waits that go with the untracked stream.
+// reductions over lane groups and the waits that go with the untracked stream.
 #pragma once
 
 #include "mfma_layout.h"
@@ -74,6 +74,30 @@ __device__ __forceinline__ void buffer_load_lds4(i32x4 rsrc, unsigned lds_base, 
         : "memory");
 }
 
+// The end of one row's online softmax, in base 2.  The running sum sx holds
+// every column but the target's: sx = sum_{v != y} 2^(z_v - m), with m the
+// (lazily re-based) running maximum and zy the target's logit.  Adding the
+// target's term 2^(zy - m) only here gives p_y - 1 = -sx / s and the row loss
+// without cancellation even where the target holds nearly all of the
+// probability: loss = log(1 + sx / e_y) then, (m - zy) ln 2 + ln s otherwise.
+// An invalid target (tok false) has no target term: NaN loss, no one-hot term.
+struct RowEnd {
+    float lse2;   // log-sum-exp, base 2
+    float loss;   // row loss, nats
+    float py1;    // p_y - 1 (0 without a valid target)
+    float inv_s;  // 1 / sum_v 2^(z_v - m)
+};
+__device__ __forceinline__ RowEnd finish_row(float m, float sx, float zy, bool tok) {
+    const float ey = tok ? __builtin_amdgcn_exp2f(zy - m) : 0.f;
+    const float s = sx + ey;
+    RowEnd o;
+    o.lse2 = m + __log2f(s);
+    o.inv_s = 1.f / s;
+    o.py1 = tok ? -sx * o.inv_s : 0.f;
+    o.loss = !tok ? __int_as_float(0x7fc00000) : (ey > sx ? log1pf(sx / ey) : ((m - zy) + __log2f(s)) * kLn2);
+    return o;
+}
+
 // All-lane reductions over each 16-lane row of the wave (DPP: quad
 // permutations, then rotations by 4 and 8 inside the row).
 template <int CTRL>
@@ -120,6 +144,16 @@ __device__ __forceinline__ float group_sum(float x) {
     return N == 16 ? row16_sum(x) : row8_sum(x);
 }
 
+// The lane index, produced by a volatile instruction: an address computed
+// from it cannot be hoisted out of a loop, so it is recomputed (a few cheap
+// instructions) where it is used instead of holding a register for the whole
+// loop (the widest passes have none to spare).
+__device__ __forceinline__ int lane_now() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
+
 __device__ __forceinline__ unsigned lds_addr(LDS_AS char* p) {
     return __builtin_amdgcn_readfirstlane((unsigned)(unsigned long long)p);
 }
@@ -148,11 +182,12 @@ struct ChunkStream {
     }
 
     // buffer resource of the chunk starting at row y0; rows at or beyond nY
-    // read as zeros
+    // read as zeros.  The range covers this chunk only: one over all remaining
+    // rows would pass 2^32 bytes (and wrap) for long matrices.
     __device__ __forceinline__ static i32x4 rsrc(const bf16* __restrict__ Y, int nY, int d, int y0) {
-        const int rows = nY - y0;
+        const int rows = nY - y0 < layout::YC ? nY - y0 : layout::YC;
         const unsigned rem = rows > 0 ? (unsigned)rows * (unsigned)d * 2u : 0u;
-        return make_rsrc(Y + (long long)y0 * d, rem);
+        return make_rsrc(Y + (long long)(rows > 0 ? y0 : 0) * d, rem);
     }
 
     // instructions [Q0, Q1) of the stream of one chunk into `slice`

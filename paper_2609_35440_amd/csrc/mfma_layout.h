@@ -1,4 +1,5 @@
-// LDS layout of the streamed chunks of the matrix-core passes (k_mfma.hip).
+// LDS layout of the streamed chunks of the matrix-core passes with a second
+// product (k_mfma.hip), and the tiled copy the other passes stream.
 //
 // Plain integer arithmetic, callable from host and device, so that the host
 // test tests/test_mfma_layout.py can compile exactly these functions and
@@ -34,6 +35,15 @@ struct Geo {
     static constexpr int NV = PADDED ? (NI >> KS) : NI;     // distinct per-lane stream offsets
     static_assert(DS % 32 == 0 && DS >= 32 && DS <= 512, "slice width");
 };
+
+// Tiled copy of a streamed matrix (the layout tiled_elems sizes), streamed by
+// the passes that read their operand straight into registers: 16-byte
+// granule o of chunk c holds row 16 c + tile_row(o), columns tile_col(o) ..
+// tile_col(o) + 7.  A wave that loads 16 bytes per lane at granule 64 b + lane
+// receives the A operand of a 16x16x32 MFMA over columns 32 b .. 32 b + 31
+// (row lane % 16, columns 32 b + 8 (lane / 16) .. + 7).
+SOLO_HD int tile_row(int o) { return o & 15; }
+SOLO_HD int tile_col(int o) { return 32 * (o >> 6) + 8 * ((o & 63) >> 4); }
 
 // Byte offset of 16-byte granule g (columns 8 g .. 8 g + 7 of the slice) of
 // streamed row r (0..15) inside a wave's chunk slice.

@@ -34,8 +34,17 @@ struct Plan {
     int rg_lo = 0, rg_hi = 0;  // modules of the readout-gradient pass
     int bg_lo = 0, bg_hi = 0;  // modules of the bias-gradient pass
     int hg_lo = 0, hg_hi = 0;  // modules whose gain-scaled copy the matrix-core gradient passes stream
-    size_t rstd = 0, lse = 0, rowloss = 0, rowrec = 0, rowdtau = 0, dgp = 0, hg = 0, total = 0;
+    int nhead_tiles = 0;       // tiled copies of the heads' readouts (0: the heads read W's copy)
+    size_t rstd = 0, lse = 0, rowloss = 0, rowrec = 0, rowdtau = 0, dgp = 0, hg = 0;
+    size_t wtile = 0, whtile = 0, total = 0;
 };
+
+// Which passes stream tiled copies: every pass of the wide tiling; in the
+// 16-row tiling the passes without a second product (exit evaluation, bias
+// gradient), which read their operand straight into registers.  The others
+// (and the vector-ALU family) read the row-major matrices.
+bool tiled_readout(const Plan& P) { return P.wide || (P.mfma && P.eval); }
+bool tiled_rgrad(const Plan& P) { return P.wide; }
 
 // Sizes, dtype and flags only (no pointer is dereferenced).
 bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
@@ -56,6 +65,16 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
     off = align_up(off + kt * 4);
     P->rowloss = off;
     off = align_up(off + kt * 4);
+    // tiled copies of the readouts the local-loss pass and exit evaluation
+    // stream: the terminal's W, and the heads' own matrix or matrices
+    if (tiled_readout(*P)) {
+        const size_t tv = (size_t)solo::tiled_elems(a.V, d) * 2;
+        P->nhead_tiles = (a.Wbar && K > 1) ? (a.readout_per_head ? K - 1 : 1) : 0;
+        P->wtile = off;
+        off = align_up(off + tv);
+        P->whtile = off;
+        off = align_up(off + tv * P->nhead_tiles);
+    }
     if (eval) {
         P->total = off;
         return true;
@@ -94,9 +113,9 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
         P->hg_hi = rg && bg ? (P->rg_hi > P->bg_hi ? P->rg_hi : P->bg_hi) : (rg ? P->rg_hi : P->bg_hi);
     }
     P->rowrec = off;
-    off = align_up(off + ((P->mfma && second) ? kt * 16 : 0));
+    off = align_up(off + (second ? kt * 16 : 0));
     P->hg = off;
-    off = align_up(off + (size_t)(P->hg_hi - P->hg_lo) * T * d * 2);
+    off = align_up(off + (size_t)(P->hg_hi - P->hg_lo) * (size_t)solo::tiled_elems(T, d) * 2);
     P->rowdtau = off;
     off = align_up(off + (a.dtau ? kt * 4 : 0));
     P->dgp = off;
@@ -162,6 +181,9 @@ int run(const solo_readout_args& x, bool eval) {
     // heads: W itself, one shared matrix, or one per head
     a.Wh = x.Wbar ? x.Wbar : x.W;
     a.wh_stride = (x.Wbar && x.readout_per_head) ? (long long)V * d : 0;
+    a.Wtt = ws + P.wtile;
+    a.Wht = P.nhead_tiles ? ws + P.whtile : ws + P.wtile;
+    a.wht_stride = P.nhead_tiles > 1 ? solo::tiled_elems(V, d) : 0;
     a.hg = ws + P.hg;
     a.hg_m0 = P.hg_lo;
     a.gain = x.gain;
@@ -172,7 +194,7 @@ int run(const solo_readout_args& x, bool eval) {
     a.rstd = (const float*)(ws + P.rstd);
     a.lse = (float*)(ws + P.lse);
     a.rowloss = x.row_loss ? x.row_loss : (float*)(ws + P.rowloss);
-    a.rowrec = (!eval && P.mfma && (P.rg_hi > P.rg_lo || P.bg_hi > P.bg_lo)) ? (float*)(ws + P.rowrec) : nullptr;
+    a.rowrec = (!eval && (P.rg_hi > P.rg_lo || P.bg_hi > P.bg_lo)) ? (float*)(ws + P.rowrec) : nullptr;
     a.rowdtau = (!eval && x.dtau) ? (float*)(ws + P.rowdtau) : nullptr;
     a.top1 = eval ? x.top1 : nullptr;
     a.dh = eval ? nullptr : x.dh;
@@ -187,9 +209,19 @@ int run(const solo_readout_args& x, bool eval) {
         return hipEventRecord((hipEvent_t)x.stage_events[stage], s) == hipSuccess;
     };
     const int dt = x.dtype;
-    if (solo::launch_row_rstd(dt, x.h, (float*)(ws + P.rstd), (long long)K * T, d, x.eps, s) != hipSuccess ||
-        !mark(0))
+    // a failure left pending by earlier work on this thread is not this call's
+    (void)hipGetLastError();
+    if (solo::launch_row_rstd(dt, x.h, (float*)(ws + P.rstd), (long long)K * T, d, x.eps, s) != hipSuccess)
         return SOLO_ERR_HIP;
+    if (tiled_readout(P)) {
+        if (solo::launch_tile((const solo::bf16*)x.W, 0, nullptr, 0, (solo::bf16*)(ws + P.wtile), 1, V, d, s) !=
+            hipSuccess)
+            return SOLO_ERR_HIP;
+        if (P.nhead_tiles && solo::launch_tile((const solo::bf16*)x.Wbar, (long long)V * d, nullptr, 0,
+                                               (solo::bf16*)(ws + P.whtile), P.nhead_tiles, V, d, s) != hipSuccess)
+            return SOLO_ERR_HIP;
+    }
+    if (!mark(0)) return SOLO_ERR_HIP;
     hipError_t e;
     if (eval)
         e = P.wide   ? solo::launch_exit_eval_mfma_wide(a, s)
@@ -203,9 +235,20 @@ int run(const solo_readout_args& x, bool eval) {
     if (solo::launch_module_sum(a.rowloss, x.losses, K, T, 1.0 / (double)T, s) != hipSuccess) return SOLO_ERR_HIP;
     if (a.rowdtau && solo::launch_module_sum(a.rowdtau, x.dtau, K, T, 1.0, s) != hipSuccess) return SOLO_ERR_HIP;
     if (!mark(2)) return SOLO_ERR_HIP;
-    if (!eval && P.hg_hi > P.hg_lo &&
-        solo::launch_prep_hg((const solo::bf16*)x.h, (const solo::bf16*)x.gain, a.g_stride, (solo::bf16*)(ws + P.hg),
-                             P.hg_lo, P.hg_hi - P.hg_lo, T, d, s) != hipSuccess)
+    // the gain-scaled copies of h the gradient passes stream, module m at
+    // hg + (m - hg_lo) tiled_elems(T, d): tiled for the register-fed passes,
+    // row-major for the direct-to-LDS readout-gradient pass
+    auto gain_copies = [&](int lo, int hi, bool as_tiles) -> bool {
+        if (hi <= lo) return true;
+        const solo::bf16* src = (const solo::bf16*)x.h + (long long)lo * T * d;
+        const solo::bf16* g = (const solo::bf16*)x.gain + (long long)lo * a.g_stride;
+        solo::bf16* dst = (solo::bf16*)(ws + P.hg) + (long long)(lo - P.hg_lo) * solo::tiled_elems(T, d);
+        return (as_tiles ? solo::launch_tile(src, (long long)T * d, g, a.g_stride, dst, hi - lo, T, d, s)
+                         : solo::launch_gain_rows(src, (long long)T * d, g, a.g_stride, dst, solo::tiled_elems(T, d),
+                                                  hi - lo, T, d, s)) == hipSuccess;
+    };
+    if (!eval && P.mfma &&
+        (!gain_copies(P.rg_lo, P.rg_hi, tiled_rgrad(P)) || !gain_copies(P.bg_lo, P.bg_hi, true)))
         return SOLO_ERR_HIP;
     if (!eval && P.rg_hi > P.rg_lo) {
         a.m0 = P.rg_lo;

@@ -9,6 +9,15 @@ namespace solo {
 
 typedef __bf16 bf16;
 
+// Tiled copy of a streamed matrix Y [nY][d] (bf16), the operand layout of the
+// matrix-core passes: rows are grouped in chunks of 16, and chunk c occupies
+// 16 d contiguous elements, one 1 KiB block per 32 columns; inside a block,
+// 16-byte granule q = 16 g + r holds Y[16 c + r][32 b + 8 g .. + 7].  Lane l of
+// a wave that loads 16 bytes at block + 16 l therefore receives exactly the
+// A operand of a 16x16x32 MFMA over those 32 columns (row l % 16, columns
+// 8 (l / 16) .. + 7).  Rows past nY up to the chunk boundary are zeros.
+__host__ __device__ inline long long tiled_elems(long long nY, int d) { return (nY + 15) / 16 * 16 * (long long)d; }
+
 // Everything one fused pass needs.  The fused kernels keep a tile of
 // "stationary" rows (X) on chip and stream "streamed" rows (Y) in chunks:
 //   local-loss pass:      X = g_k * h_k (rows t),     Y = readout of module k (rows v)
@@ -17,9 +26,10 @@ typedef __bf16 bf16;
 //   bias-grad pass:       same, without the second product
 // In the matrix-core passes both products see the same rounded operands
 // bf16(g_k * h_k) and R_k: the local-loss pass rounds g_k * h_k while it loads
-// its stationary tile, and the readout-/bias-gradient passes stream a copy
-// that a small kernel wrote with the same rounding (so their recomputed
-// logits match the stored log-sum-exp).
+// its stationary tile, and the readout-/bias-gradient passes stream a tiled
+// copy that a small kernel wrote with the same rounding (so their recomputed
+// logits match the stored log-sum-exp).  The register-fed matrix-core passes
+// stream Y from its tiled copy (see tiled_elems); the others read Y row-major.
 struct FusedArgs {
     int K, T, d, V;
     int m0;               // readout-/bias-gradient passes: module of grid row 0 (module = m0 + blockIdx.y)
@@ -28,7 +38,11 @@ struct FusedArgs {
     const void* Wt;       // [V][d] elem: readout of module K-1 (the terminal)
     const void* Wh;       // elem: readout of module k < K-1 at Wh + k * wh_stride
     long long wh_stride;  // elements; 0 when every head reads the same matrix
-    const void* hg;       // [..][T][d] bf16: bf16(g_k * h_k) of modules hg_m0.. (matrix-core gradient passes)
+    const void* Wtt;      // tiled copy of Wt (register-fed matrix-core passes)
+    const void* Wht;      // tiled copy of the heads' readout(s): module k < K-1 at Wht + k * wht_stride
+    long long wht_stride; // elements; 0 when every head reads the same matrix
+    const void* hg;       // copies of bf16(g_k * h_k), modules hg_m0.., tiled_elems(T, d) apart: row-major for
+                          // the direct-to-LDS passes, tiled for the register-fed ones
     int hg_m0;
     const void* gain;     // elem: gain of module k at gain + k * g_stride
     int g_stride;         // 0 (one gain) or d (one per module)
@@ -37,7 +51,8 @@ struct FusedArgs {
     const int32_t* targets;  // [K][T]
     const float* rstd;    // [K][T] 1/sqrt(mean h^2 + eps)
     float* lse;           // [K][T] log-sum-exp of the logits (written by the local-loss pass)
-    float* rowrec;        // [K][T][4] or null: {lse log2 e, r tau log2 e, target bits, r tau / T} per token
+    float* rowrec;        // [K][T][4] or null: {lse log2 e, r tau log2 e, target bits, p_y - 1} per token
+                          // (the vector-ALU family reads only p_y - 1)
     float* rowloss;       // [K][T] per-token cross-entropy
     float* rowdtau;       // [K][T] or null: per-token share of d loss / d tau
     int32_t* top1;        // [K][T] or null: exit evaluation, argmax of the logits (lowest index on ties)
@@ -56,9 +71,14 @@ constexpr int kValuRows = 8;       // stationary rows per workgroup (vector-ALU 
 
 // small kernels (k_small.hip)
 hipError_t launch_row_rstd(int dtype, const void* h, float* rstd, long long rows, int d, float eps, hipStream_t s);
-// hg[m][t][j] = bf16(h[m0 + m][t][j] * gain[(m0 + m) g_stride + j]) for m in [0, nmod)
-hipError_t launch_prep_hg(const bf16* h, const bf16* gain, int g_stride, bf16* hg, int m0, int nmod, int T, int d,
-                          hipStream_t s);
+// tiled copies (layout of tiled_elems) of nmat row-major matrices [nY][d], src_stride
+// elements apart; with a gain, of bf16(Y * gain[m g_stride + j]) (the rounding of the
+// local-loss pass's stationary tile)
+hipError_t launch_tile(const bf16* src, long long src_stride, const bf16* gain, int g_stride, bf16* dst, int nmat,
+                       int nY, int d, hipStream_t s);
+// row-major copies hg[m][t][j] = bf16(h[m][t][j] gain[m g_stride + j]), matrices src_stride / dst_stride apart
+hipError_t launch_gain_rows(const bf16* h, long long src_stride, const bf16* gain, int g_stride, bf16* hg,
+                            long long dst_stride, int nmat, int T, int d, hipStream_t s);
 // out[k] = scale * sum_t rows[k][t], fixed order
 hipError_t launch_module_sum(const float* rows, float* out, int K, int T, double scale, hipStream_t s);
 // dgain[slot][j] = sum over tiles of part[slot][tile][j], fixed order

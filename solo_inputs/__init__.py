@@ -27,6 +27,7 @@ __all__ = [
     "zipf_targets",
     "make_inputs",
     "make_extras",
+    "make_profile_inputs",
 ]
 
 
@@ -78,6 +79,9 @@ CONFIGS: Dict[str, Config] = {
 # tensor ids inside one (seed, config) stream family
 _H, _W, _GAIN, _TARGETS, _HOT = 0, 1, 2, 3, 4
 _GAIN_K, _WBAR, _TAU, _BIAS = 5, 6, 7, 8
+_DIR, _PH, _PW, _PT = 9, 10, 11, 12
+# stream family of the structured inputs (make_profile_inputs)
+_PROFILE_ID = 100
 
 
 def _rng(seed: int, config_id: int, tensor_id: int) -> np.random.Generator:
@@ -230,4 +234,44 @@ def make_extras(x: dict, seed: int = 0, *, per_module_gain: bool = False, wbar: 
     out["tau"] = (np.float32(0.5) + np.float32(1.5) * _rng(seed, cfg.config_id, _TAU).random(K, dtype=np.float32)
                   ) if tau else None
     out["bias"] = _normal_f32(_rng(seed, cfg.config_id, _BIAS), (K, V), 0.5) if bias else None
+    return out
+
+
+def make_profile_inputs(dtype: str, K: int, T: int, d: int, V: int, profile: np.ndarray, targets: np.ndarray,
+                        seed: int = 0, row_jitter: float = 0.1, w_noise: float = 0.02) -> dict:
+    """Structured inputs whose logits follow a chosen profile over the vocabulary.
+
+    A seeded random sign vector s (entries +1 or -1) is shared by the hidden
+    states and the readout rows:
+
+      h[k, t] = s * (1 + row_jitter * N(0, 1))          (elementwise)
+      gain    = 1 + 0.1 * N(0, 1)
+      W[v]    = profile[v] * s / d + N(0, w_noise^2)
+
+    so that a row's logit at column v is close to ``profile[v]`` (the hidden
+    states have root-mean-square close to one and the gain close to one), with
+    seeded noise of a few tenths that makes every row and column different.
+    Profiles that climb by many nats across the vocabulary, or that put one
+    column far above the others, steer the online softmax through re-basing
+    and through rows whose target holds nearly all of the probability.
+    ``targets`` [K, T] (int32) is used as given.  Returns the keys of
+    make_inputs (a Config named "profile" of the given sizes and dtype).
+    """
+    cfg = Config("profile", _PROFILE_ID, K=K, T=T, d=d, V=V, dtype=dtype)
+    profile = np.asarray(profile, dtype=np.float32)
+    if profile.shape != (V,) or targets.shape != (K, T):
+        raise ValueError("profile must be [V] and targets [K, T]")
+    sgn = np.where(_rng(seed, _PROFILE_ID, _DIR).random(d) < 0.5, -1.0, 1.0).astype(np.float32)
+    h = sgn[None, None, :] * (np.float32(1.0) + _normal_f32(_rng(seed, _PROFILE_ID, _PH), (K, T, d), row_jitter))
+    gain = np.float32(1.0) + _normal_f32(_rng(seed, _PROFILE_ID, _GAIN), (d,), 0.1)
+    W = profile[:, None] * sgn[None, :] / np.float32(d) + _normal_f32(_rng(seed, _PROFILE_ID, _PW), (V, d), w_noise)
+    out = {"cfg": cfg, "targets": np.ascontiguousarray(targets, dtype=np.int32)}
+    if dtype == "bf16":
+        for name, a in (("h", h), ("gain", gain), ("W", W)):
+            out[name + "_bits"] = bf16_bits(a.astype(np.float32))
+            out[name] = bf16_from_bits(out[name + "_bits"])
+    elif dtype == "f32":
+        out["h"], out["gain"], out["W"] = (np.ascontiguousarray(a, dtype=np.float32) for a in (h, gain, W))
+    else:
+        raise ValueError(f"unknown dtype {dtype!r}")
     return out

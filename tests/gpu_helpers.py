@@ -55,6 +55,47 @@ def run_gpu(x: dict, final_module_dW: bool = True, eps: float = 1e-6, dev_inputs
     return res
 
 
+def row_loss_error_bound(h, gain, R, targets, tau, dtype, bias=None, eps=1e-6):
+    """Per-token bound on |row_loss_gpu - row_loss_oracle| of one module.
+
+    The matrix-core kernels multiply the stored readout R by bf16(g * h_t), the
+    exact product of two bf16 values rounded once to nearest even, and
+    accumulate in fp32; the vector-ALU kernels multiply in fp32.  Write
+    e_tj = rounded_tj - g_j h_tj for the operand's rounding.  The kernel's
+    logit then differs from the exact one by
+        tau r_t sum_j R_vj e_tj                      (the operand's rounding, exact)
+      + tau r_t (an fp32 accumulation error of at most gamma sum_j |R_vj rounded_tj|)
+    where gamma = n 2^-24 for n roundings along the accumulation: one per
+    32-deep matrix instruction, the split-K tree and the scalings (d / 32 + 8)
+    on the matrix cores, d for the vector-ALU kernels' sequential sums.  With
+    B_tv the absolute value of the first term plus the second, a row loss
+    lse_t - z_{t,y} moves by at most max_v B_tv (the log-sum-exp is
+    1-Lipschitz in the largest change) plus B_{t,y}; the exp2/log2
+    instructions and the fp32 bias add contribute a relative 2^-20 of the
+    largest logit and of the loss.  Returns the bound per token, [T].
+    """
+    h = np.asarray(h, np.float64)
+    g = np.asarray(gain, np.float64)
+    R = np.asarray(R, np.float64)
+    exact = h * g
+    d = h.shape[-1]
+    if dtype == "bf16":
+        from solo_inputs import round_bf16
+
+        rounded = round_bf16(exact.astype(np.float32)).astype(np.float64)
+        gamma = (d / 32 + 8) * 2.0 ** -24
+    else:
+        rounded = exact.astype(np.float32).astype(np.float64)
+        gamma = d * 2.0 ** -24
+    r = 1.0 / np.sqrt(np.mean(h * h, axis=-1) + eps)
+    scale = tau * r[:, None]
+    B = scale * (np.abs((rounded - exact) @ R.T) + gamma * (np.abs(rounded) @ np.abs(R).T))   # [T, V]
+    z = scale * (exact @ R.T) + (0.0 if bias is None else np.asarray(bias, np.float64)[None, :])
+    rows = np.arange(h.shape[0])
+    zabs = np.abs(z).max(axis=1)
+    return B.max(axis=1) + B[rows, np.asarray(targets)] + 2.0 ** -20 * (1.0 + 2.0 * zabs)
+
+
 def rel_max_err(a, b) -> float:
     a = np.asarray(a, np.float64)
     b = np.asarray(b, np.float64)

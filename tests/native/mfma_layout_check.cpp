@@ -1,9 +1,16 @@
-// Host check of the LDS layout used by the matrix-core passes: emulate the
-// direct-to-LDS stream of one chunk slice with the functions of
-// mfma_layout.h, then every row-wise and transposing operand read, and check
-// that each returns the element its MFMA operand needs.  Also counts LDS bank
-// conflicts of both read patterns with the service model measured on gfx950:
-// a 16-byte-per-lane read is served 8 lanes at a time over 32 banks of 4
+// Host check of the data layouts of the matrix-core passes, with the same
+// headers the kernels include:
+//   - 16-row tiling, passes with a second product: emulate the direct-to-LDS
+//     stream of one chunk slice, then every row-wise and transposing operand
+//     read, and check that each returns the element its MFMA operand needs;
+//   - the tiled copy the register-fed passes stream (mfma_layout.h tile_row /
+//     tile_col): the 16 bytes a lane loads at k-step kk are the A operand of
+//     the 16x16x32 logit product (row lane % 16, columns 32 kk + 8 (lane / 16)
+//     .. + 7 of the wave's slice);
+//   - the wide tiling: each wave writes those operand registers into its LDS
+//     slice and reads it back with the transposing read of its second product.
+// Also counts LDS bank conflicts with the service model measured on gfx950:
+// a 16-byte-per-lane access is served 8 lanes at a time over 32 banks of 4
 // bytes, the 8-byte transposing read 32 lanes at a time over 64 banks.
 // Transposing read semantics (ds_read_b64_tr_b16, per 16-lane group): lane i
 // receives, as element y, the 16-bit value (i % 4) of the 8 bytes addressed by
@@ -33,6 +40,27 @@ static int conflicts(const int* addr, int width, int pass, int nbanks) {
         extra += worst - 1;
     }
     return extra;
+}
+
+// The operand a lane of wave w (DS columns per wave) holds after loading
+// k-step kk of a chunk from the tiled copy: (row, column) of element e.
+template <int DS>
+static std::pair<int, int> loaded(int w, int kk, int lane, int e) {
+    const int o = w * (DS / 32) * 64 + kk * 64 + lane;  // granule index inside the chunk
+    return {tile_row(o), tile_col(o) + e};
+}
+
+// The tiled copy hands every lane of every wave its logit-product operand.
+template <int DS, int NWAVES>
+int check_tiled() {
+    int errors = 0;
+    for (int w = 0; w < NWAVES; ++w)
+        for (int kk = 0; kk < DS / 32; ++kk)
+            for (int l = 0; l < 64; ++l)
+                for (int e = 0; e < 8; ++e)
+                    if (loaded<DS>(w, kk, l, e) != std::pair<int, int>{l & 15, w * DS + 32 * kk + 8 * (l >> 4) + e})
+                        ++errors;
+    return errors;
 }
 
 // NWAVES waves of DS columns each cover the row width d = NWAVES DS.
@@ -99,60 +127,53 @@ template <int DS, int NWAVES = NW>
 int report() {
     int cr = 0, ct = 0;
     const int e = check<DS, NWAVES>(cr, ct);
-    std::printf("DS=%d waves=%d padded=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d\n", DS, NWAVES,
-                (int)Geo<DS>::PADDED, Geo<DS>::SLICE, e, cr, ct);
-    return e;
+    const int et = check_tiled<DS, NWAVES>();
+    std::printf("DS=%d waves=%d padded=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d tiled_errors=%d\n", DS,
+                NWAVES, (int)Geo<DS>::PADDED, Geo<DS>::SLICE, e, cr, ct, et);
+    return e + et;
 }
 
 
-// The wide layout (mfma_layout_wide.h): staged register -> LDS writes of one
-// wave slice, the row-wise reads of the 16x16x32 logit product and the
-// transposing reads of the 16x16x16 second product.
+// The wide layout (mfma_layout_wide.h): the operand registers of k-step kk
+// written at the row-wise read offset of the slice, and the transposing reads
+// of the 16x16x16 second product.
 template <int DS>
-int check_wide(int& conflicts_row, int& conflicts_tr, int& conflicts_wr) {
+int check_wide(int& conflicts_wr, int& conflicts_tr) {
     namespace W = solo::layoutw;
     using G = W::Geo<DS>;
     int errors = 0;
-    conflicts_row = conflicts_tr = conflicts_wr = 0;
-    std::map<int, std::pair<int, int>> lds;  // LDS byte -> (row, column within the slice)
-    for (int q = 0; q < G::NI; ++q) {
-        int addr[64];
-        for (int p = 0; p < 64; ++p) {
-            const int row = W::stage_row<DS>(q, p), gran = W::stage_gran<DS>(q, p);
-            const int a = W::stage_dst<DS>(q, p);
-            addr[p] = a;
-            if (row < 0 || row >= 16 || a < 0 || a + 16 > G::SLICE) ++errors;
-            for (int e = 0; e < 8; ++e) {
-                if (lds.count(a + 2 * e)) ++errors;
-                lds[a + 2 * e] = {row, 8 * gran + e};
+    conflicts_wr = conflicts_tr = 0;
+    for (int w = 0; w < W::NW; ++w) {
+        const int js = w * DS;
+        std::map<int, std::pair<int, int>> lds;  // LDS byte -> (row, column within the slice)
+        for (int kk = 0; kk < DS / 32; ++kk) {
+            int addr[64];
+            for (int l = 0; l < 64; ++l) {
+                const int a = W::rowread_off<DS>(l, kk);
+                addr[l] = a;
+                if (a < 0 || a + 16 > G::SLICE) ++errors;
+                for (int e = 0; e < 8; ++e) {
+                    const std::pair<int, int> v = loaded<DS>(w, kk, l, e);
+                    if (v != std::pair<int, int>{l & 15, js + 32 * kk + 8 * (l >> 4) + e}) ++errors;
+                    if (lds.count(a + 2 * e)) ++errors;
+                    lds[a + 2 * e] = {v.first, v.second - js};
+                }
             }
+            conflicts_wr += conflicts(addr, 16, 8, 32);
         }
-        conflicts_wr += conflicts(addr, 16, 8, 32);
-    }
-    if ((int)lds.size() != 16 * DS) ++errors;
-    for (int kk = 0; kk < DS / 32; ++kk) {
-        int addr[64];
-        for (int l = 0; l < 64; ++l) {
-            addr[l] = W::rowread_off<DS>(l, kk);
-            for (int e = 0; e < 8; ++e) {
-                auto it = lds.find(addr[l] + 2 * e);
-                std::pair<int, int> want{l & 15, 32 * kk + 8 * (l >> 4) + e};
-                if (it == lds.end() || it->second != want) ++errors;
-            }
-        }
-        conflicts_row += conflicts(addr, 16, 8, 32);
-    }
-    for (int b = 0; b < DS / 16; ++b) {
-        int addr[64];
-        for (int l = 0; l < 64; ++l) addr[l] = W::trread_off<DS>(l, b);
-        conflicts_tr += conflicts(addr, 8, 32, 64);
-        for (int l = 0; l < 64; ++l) {
-            const int grp = l / 16, i = l % 16;
-            for (int e = 0; e < 4; ++e) {
-                const int src = grp * 16 + 4 * e + i / 4;
-                auto it = lds.find(addr[src] + 2 * (i % 4));
-                std::pair<int, int> want{4 * grp + e, 16 * b + i};  // A[m = column][k = row] of the 16x16x16 product
-                if (it == lds.end() || it->second != want) ++errors;
+        if ((int)lds.size() != 16 * DS) ++errors;
+        for (int b = 0; b < DS / 16; ++b) {
+            int addr[64];
+            for (int l = 0; l < 64; ++l) addr[l] = W::trread_off<DS>(l, b);
+            conflicts_tr += conflicts(addr, 8, 32, 64);
+            for (int l = 0; l < 64; ++l) {
+                const int grp = l / 16, i = l % 16;
+                for (int e = 0; e < 4; ++e) {
+                    const int src = grp * 16 + 4 * e + i / 4;
+                    auto it = lds.find(addr[src] + 2 * (i % 4));
+                    std::pair<int, int> want{4 * grp + e, 16 * b + i};  // A[m = column][k = row] of the 16x16x16 product
+                    if (it == lds.end() || it->second != want) ++errors;
+                }
             }
         }
     }
@@ -161,10 +182,10 @@ int check_wide(int& conflicts_row, int& conflicts_tr, int& conflicts_wr) {
 
 template <int DS>
 int report_wide() {
-    int cr = 0, ct = 0, cw = 0;
-    const int e = check_wide<DS>(cr, ct, cw);
-    std::printf("WIDE DS=%d slice=%d errors=%d row_conflicts=%d tr_conflicts=%d write_conflicts=%d\n", DS,
-                solo::layoutw::Geo<DS>::SLICE, e, cr, ct, cw);
+    int cw = 0, ct = 0;
+    const int e = check_wide<DS>(cw, ct);
+    std::printf("WIDE DS=%d slice=%d errors=%d write_conflicts=%d tr_conflicts=%d\n", DS,
+                solo::layoutw::Geo<DS>::SLICE, e, cw, ct);
     return e;
 }
 
@@ -178,10 +199,6 @@ int main() {
     e += report<192>();
     e += report<224>();
     e += report<256>();
-    // one-wave-per-SIMD kernels: 4 waves of d / 4 columns
-    e += report<256, 4>();
-    e += report<384, 4>();
-    e += report<512, 4>();
     // the wide layout: 8 waves of d / 8 columns; 320 is the shipped width (d = 2560)
     e += report_wide<320>();
     e += report_wide<384>();

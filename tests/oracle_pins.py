@@ -13,6 +13,7 @@ What pins what:
   * T = 1, V = 2 -> loss = softplus(z_other - z_target)
   * V = 1 -> loss 0 and every gradient 0
   * invariants I1..I6 and softmax rows summing to one
+  * torch fp64 softmax -> softmax_rows (ordinary, shifted to 1000, dominant entry)
   * the unblocked brute force agrees to 1e-12
 """
 from __future__ import annotations
@@ -198,6 +199,21 @@ def pin_invariants(orc, seed=5):
     np.testing.assert_allclose(p.sum(1), 1.0, rtol=0, atol=1e-15)
 
 
+def pin_softmax_rows(orc, seed=8):
+    """softmax_rows against torch's fp64 softmax (a library routine), on
+    ordinary logits, on logits near 1000 (where an unshifted exp overflows) and
+    on a row with one dominant entry."""
+    import torch
+
+    rng = np.random.default_rng(seed)
+    z = rng.standard_normal((5, 9)) * 3.0
+    for zz in (z, z + 1000.0, np.concatenate([z[:1], [[40.0] + [0.0] * 8]])):
+        ref = torch.softmax(torch.from_numpy(zz), dim=-1).numpy()
+        got = orc.softmax_rows(zz)
+        assert np.all(np.isfinite(got)), "softmax_rows not finite"
+        assert np.abs(got - ref).max() <= 1e-14, ("softmax_rows", np.abs(got - ref).max())
+
+
 def pin_bruteforce(orc, eps=1e-6, seed=6):
     h, gain, W, y = tiny_case(seed, K=2, T=4, d=6, V=5)
     a = orc.readout_fwd_bwd(h, gain, W, y, True, eps, row_chunk=3)
@@ -226,4 +242,5 @@ ALL_PINS = [
     pin_invariants,
     pin_bruteforce,
     pin_row_subset,
+    pin_softmax_rows,
 ]

@@ -50,28 +50,38 @@ def al(x):
     return (x + 255) // 256 * 256
 
 
+def tiled(n, d):
+    # bytes of a bf16 tiled copy of an [n][d] matrix: rows padded to chunks of 16
+    return -(-n // 16) * 16 * d * 2
+
+
 def test_workspace_has_no_TV_term():
     # bf16 matrix-core families: rstd, lse, row_loss (3 K T 4) + per-token records of
-    # every module (K T 16) + the terminal's gain-gradient partials (one row of d fp32
-    # per token tile: 64-row tiles at d <= 1024, 32-row tiles up to 2048, 16-row tiles
-    # at d = 2560) + the terminal's bf16 copy of gain * h (T d 2); no V x d and no T x V piece
+    # every module (K T 16) + the terminal's bf16 copy of gain * h (T d 2, rows padded
+    # to chunks of 16) + its gain-gradient partials (one row of d fp32 per token tile:
+    # 64-row tiles at d <= 1024, 32-row tiles up to 2048, 16-row tiles at d = 2560).
+    # The wide tiling (d = 2560) also streams a tiled copy of the readout (V d 2).
+    # No T x V piece.
     for K, T, d, V, rows in [(4, 16384, 2048, 32000, 32), (2, 32768, 2048, 128256, 32), (4, 8192, 1024, 32000, 64),
                              (1, 1, 256, 1, 64), (3, 100, 1536, 50, 32), (8, 16384, 2560, 32000, 16)]:
-        want = 3 * al(K * T * 4) + al(K * T * 16) + al(-(-T // rows) * d * 4) + al(T * d * 2)
+        wt = al(tiled(V, d)) if d == 2560 else 0
+        want = 3 * al(K * T * 4) + wt + al(K * T * 16) + al(tiled(T, d)) + al(-(-T // rows) * d * 4)
         assert B.workspace_size(K, T, d, V, B.SOLO_BF16, True) == want
-        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == 3 * al(K * T * 4)
-    # the workspace does not depend on V at all
-    assert B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True) == \
-        B.workspace_size(4, 16384, 2048, 128256, B.SOLO_BF16, True)
-    # doubling T grows it by K T (12 + 16) + (T/32) d 4 + T d 2 bytes
+        assert B.workspace_size(K, T, d, V, B.SOLO_BF16, False) == 3 * al(K * T * 4) + wt
+    # the 16-row tiling's workspace does not depend on V at all; the wide tiling's
+    # only through the readout copy
     a = B.workspace_size(4, 16384, 2048, 32000, B.SOLO_BF16, True)
+    assert B.workspace_size(4, 16384, 2048, 128256, B.SOLO_BF16, True) == a
+    aw = B.workspace_size(8, 16384, 2560, 32000, B.SOLO_BF16, True)
+    assert B.workspace_size(8, 16384, 2560, 64000, B.SOLO_BF16, True) - aw == 32000 * 2560 * 2
+    # doubling T grows it by K T (12 + 16) + (T/32) d 4 + T d 2 bytes
     b = B.workspace_size(4, 32768, 2048, 32000, B.SOLO_BF16, True)
     assert b - a == 4 * 16384 * 28 + 512 * 2048 * 4 + 16384 * 2048 * 2
     # well below one module's T x V fp32 logits (2.1 GB at the 1B shape)
     assert a < 16384 * 32000 * 4 / 20
-    # vector-ALU family: 8-row token tiles, no per-token records
+    # vector-ALU family: 8-row token tiles, per-token records (p_y - 1 for the readout-gradient pass)
     K, T, d, V = 2, 256, 64, 512
-    assert B.workspace_size(K, T, d, V, B.SOLO_F32, True) == 3 * al(K * T * 4) + al(-(-T // 8) * d * 4)
+    assert B.workspace_size(K, T, d, V, B.SOLO_F32, True) == 3 * al(K * T * 4) + al(K * T * 16) + al(-(-T // 8) * d * 4)
     # invalid arguments -> 0
     assert B.workspace_size(0, 8, 64, 32, B.SOLO_BF16, True) == 0
     assert B.workspace_size(1, 8, 63, 32, B.SOLO_BF16, True) == 0
@@ -180,23 +190,30 @@ def test_general_workspace_sizes():
     K, T, d, V = 3, 40, 256, 100
     kt = K * T
     tiles = -(-T // 64)  # 64-row token tiles of the matrix-core kernels at d <= 1024
+    wt = al(tiled(V, d))  # a tiled copy of a readout (exit evaluation streams it)
     head = B.workspace_size(K, T, d, V, B.SOLO_BF16, True)
     # the headline arguments through the general entry point: same workspace
     assert B.general_workspace_size(gargs()) == head
     # per-module gains: one partial slot per module
     assert B.general_workspace_size(gargs(gain_per_module=1)) == \
-        3 * al(kt * 4) + al(kt * 16) + al(K * tiles * d * 4) + al(T * d * 2)
+        3 * al(kt * 4) + al(kt * 16) + al(tiled(T, d)) + al(K * tiles * d * 4)
     # temperature gradient: per-token shares
     assert B.general_workspace_size(gargs(dtau=P)) == head + al(kt * 4)
     # bias gradient without any readout gradient: records and gain * h copies of all K
     # modules for the bias-gradient pass, no gain partials
     assert B.general_workspace_size(gargs(final_module_dW=0, dW=0, dgain=0, dbias=P)) == \
-        3 * al(kt * 4) + al(kt * 16) + al(K * T * d * 2)
+        3 * al(kt * 4) + al(kt * 16) + al(K * tiled(T, d))
+    # a separate copy for the heads: the local-loss pass reads it in place
+    assert B.general_workspace_size(gargs(Wbar=P)) == head
     # PRIV: every module's copy
     assert B.general_workspace_size(gargs(heads_train_readout=1, readout_per_head=1, Wbar=P, dWbar=P)) == \
-        head - al(T * d * 2) + al(K * T * d * 2)
-    # exit evaluation: per-token statistics only
-    assert B.exit_eval_workspace_size(gargs()) == 3 * al(kt * 4)
+        head - al(tiled(T, d)) + al(K * tiled(T, d))
+    # exit evaluation: per-token statistics and the tiled readout it streams; with one
+    # readout per head, one tiled copy each
+    assert B.exit_eval_workspace_size(gargs()) == 3 * al(kt * 4) + wt
+    assert B.exit_eval_workspace_size(gargs(readout_per_head=1, Wbar=P)) == 3 * al(kt * 4) + wt + al((K - 1) * tiled(V, d))
+    # the vector-ALU family (fp32) reads the row-major readout: no tiled copies
+    assert B.exit_eval_workspace_size(gargs(dtype=B.SOLO_F32)) == 3 * al(kt * 4)
     # rejected flags -> 0
     assert B.general_workspace_size(gargs(gain_per_module=2)) == 0
     assert B.general_workspace_size(gargs(K=0)) == 0

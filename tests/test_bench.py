@@ -18,10 +18,16 @@ def test_more_than_one_gpu_is_refused_with_a_message():
 
 
 def test_source_stamp_ignores_comments_and_whitespace_only():
-    files = {f: open(os.path.join(ROOT, "paper_2609_35440_amd", "csrc", f)).read()
-             for f in ("k_mfma.hip", "mfma_common.h", "mfma_layout.h", "solo_internal.h")}
+    csrc = os.path.join(ROOT, "paper_2609_35440_amd", "csrc")
+    names = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    # every library source is stamped, the wide tiling and the small kernels included
+    assert {"k_mfma.hip", "k_mfma_wide.hip", "mfma_layout_wide.h", "k_small.hip", "solo_api.hip"} <= set(names)
+    files = {f: open(os.path.join(csrc, f)).read() for f in names}
     base = bench.kernel_sources_hash(lambda f: files[f])
     assert base == bench.kernel_sources_hash()
+    changed_wide = dict(files)
+    changed_wide["k_mfma_wide.hip"] = files["k_mfma_wide.hip"] + "\nstatic int extra_symbol;\n"
+    assert bench.kernel_sources_hash(lambda f: changed_wide[f]) != base
     edited = dict(files)
     edited["k_mfma.hip"] = "// a new comment\n/* and a block\n comment */\n" + files["k_mfma.hip"].replace(
         "\n", "\n  ", 5)

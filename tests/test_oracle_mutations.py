@@ -27,6 +27,8 @@ MUTANTS = {
     "eps_outside_sqrt": ("r = 1.0 / np.sqrt(ms + float(eps))", "r = 1.0 / (np.sqrt(ms) + float(eps))"),
     "wrong_target_index": ("row_loss[t0:t1] = lse - z[rows, yc]", "row_loss[t0:t1] = lse - z[rows, (yc + 1) % z.shape[1]]"),
     "dW_uses_n_not_hhat": ("dW += delta.T @ hhat", "dW += delta.T @ n"),
+    "softmax_without_exp": ("e = np.exp(z - m)", "e = z - m"),
+    "softmax_without_shift": ("e = np.exp(z - m)", "e = np.exp(z)"),
     "frozen_gets_dW": [
         ("want = bool(final_module_dW) and k == K - 1", "want = bool(final_module_dW)"),
         ("dW, dgain = dWk, dgk", "dW, dgain = (dWk, dgk) if dW is None else (dW + dWk, dgain + dgk)"),
