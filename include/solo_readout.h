@@ -179,6 +179,28 @@ int solo_readout_fwd_bwd_profiled(int K, int T, int d, int V, int dtype, float e
                                   void* hip_stream, void* const* stage_events);
 
 /*
+ * solo_readout_fwd_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The workspace is a static device array
+ * inside the library, one per GPU, of solo_readout_scratch_limit() bytes
+ * (128 MiB), held from the first call on a device until the process ends.
+ * Same arguments (minus workspace), kernels, semantics and results as
+ * solo_readout_fwd_bwd, on the current device (which must own hip_stream).
+ * Errors: as solo_readout_fwd_bwd; SOLO_ERR_WORKSPACE when the call needs
+ * more workspace than the limit (solo_readout_workspace_size tells).  The
+ * function calls no allocating routine.  Every call on one GPU shares that
+ * GPU's scratch: calls that overlap on one GPU (different streams, or
+ * threads) race and must be serialised by the caller; one stream in order is
+ * safe.  Nothing in the scratch needs to start at zero.
+ */
+size_t solo_readout_scratch_limit(void);
+int solo_readout_fwd_bwd_noalloc(int K, int T, int d, int V, int dtype, float eps,
+                                 const void* h, const void* gain, const void* W,
+                                 const int32_t* targets, int final_module_dW,
+                                 float* losses, float* row_loss, void* dh,
+                                 float* dW, float* dgain, void* hip_stream);
+
+/*
  * Arguments of solo_readout_general and solo_readout_exit_eval.  Zero-fill
  * the struct, then set what the call uses; NULL pointers and 0 flags mean
  * "absent".  Sizes, dtype, eps, h, targets, losses, row_loss, workspace and

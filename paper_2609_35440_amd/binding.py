@@ -23,6 +23,8 @@ __all__ = [
     "kernel_family",
     "readout_fwd_bwd",
     "readout_fwd_bwd_raw",
+    "readout_fwd_bwd_noalloc_raw",
+    "scratch_limit",
     "SoloReadoutArgs",
     "GeneralResult",
     "EvalResult",
@@ -120,6 +122,10 @@ def load_library():
     lib.solo_readout_fwd_bwd.argtypes = common
     lib.solo_readout_fwd_bwd_profiled.restype = c_int
     lib.solo_readout_fwd_bwd_profiled.argtypes = common + [ctypes.POINTER(vp)]
+    lib.solo_readout_scratch_limit.restype = c_size
+    lib.solo_readout_scratch_limit.argtypes = []
+    lib.solo_readout_fwd_bwd_noalloc.restype = c_int
+    lib.solo_readout_fwd_bwd_noalloc.argtypes = common[:16] + [vp]
     pargs = [ctypes.POINTER(SoloReadoutArgs)]
     for name in ("solo_readout_general_workspace_size", "solo_readout_exit_eval_workspace_size"):
         getattr(lib, name).restype = c_size
@@ -175,6 +181,21 @@ def readout_fwd_bwd_raw(K, T, d, V, dtype, eps, h, gain, W, targets, final_modul
         return int(lib.solo_readout_fwd_bwd(*args))
     arr = (ctypes.c_void_p * NUM_STAGES)(*[(e or None) for e in stage_events])
     return int(lib.solo_readout_fwd_bwd_profiled(*args, arr))
+
+
+def scratch_limit() -> int:
+    """Bytes of the library's static scratch (the allocation-free entry point)."""
+    return int(load_library().solo_readout_scratch_limit())
+
+
+def readout_fwd_bwd_noalloc_raw(K, T, d, V, dtype, eps, h, gain, W, targets, final_module_dW, losses, row_loss, dh,
+                                dW, dgain, stream) -> int:
+    """solo_readout_fwd_bwd_noalloc with integer pointers (0 for NULL); returns the status code."""
+    lib = load_library()
+    return int(lib.solo_readout_fwd_bwd_noalloc(
+        int(K), int(T), int(d), int(V), int(dtype), float(eps), h or None, gain or None, W or None, targets or None,
+        int(final_module_dW), losses or None, row_loss or None, dh or None, dW or None, dgain or None,
+        stream or None))
 
 
 def _dtype_code(t):

@@ -2,6 +2,7 @@
 // layout and the launch sequence on the caller's stream.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "solo_readout.h"
 #include "solo_internal.h"
@@ -304,9 +305,60 @@ solo_readout_args headline(int K, int T, int d, int V, int dtype, float eps, con
     return a;
 }
 
+// Scratch of the entry point that allocates nothing: a file-scope device
+// array, one copy per GPU, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address): the device address is fetched once per device, with that
+// device current, and kept.
+constexpr size_t kScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (nullptr on a HIP error).
+void* scratch_of_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        scratch_ptr[dev] = ptr;
+    }
+    return scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t solo_readout_scratch_limit(void) { return kScratchBytes; }
+
+int solo_readout_fwd_bwd_noalloc(int K, int T, int d, int V, int dtype, float eps, const void* h, const void* gain,
+                                 const void* W, const int32_t* targets, int final_module_dW, float* losses,
+                                 float* row_loss, void* dh, float* dW, float* dgain, void* hip_stream) {
+    if (dtype != SOLO_BF16 && dtype != SOLO_F32) return SOLO_ERR_DTYPE;
+    if (!shape_ok(K, T, d, V)) return SOLO_ERR_SHAPE;
+    solo_readout_args a = headline(K, T, d, V, dtype, eps, h, gain, W, targets, final_module_dW, losses, row_loss,
+                                   dh, dW, dgain, nullptr, 0, hip_stream, nullptr);
+    Plan P;
+    if (!make_plan(a, false, &P)) return SOLO_ERR_SHAPE;
+    if (P.total > kScratchBytes) return SOLO_ERR_WORKSPACE;
+    // every other host check before the first HIP call (a stand-in, aligned
+    // workspace of the limit's size: only the scratch's address is unknown yet)
+    a.workspace = (void*)(uintptr_t)kAlign;
+    a.workspace_bytes = kScratchBytes;
+    const int st = check(a, false, &P);
+    if (st != SOLO_OK) return st;
+    (void)hipGetLastError();
+    void* ws = scratch_of_current_device();
+    if (!ws) return SOLO_ERR_HIP;
+    a.workspace = ws;
+    a.workspace_bytes = kScratchBytes;
+    return run(a, false);
+}
 
 int solo_readout_abi_version(void) { return SOLO_READOUT_ABI_VERSION; }
 

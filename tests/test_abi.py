@@ -29,7 +29,8 @@ def test_exports_match_header():
     assert set(names) == {"solo_readout_abi_version", "solo_status_string", "solo_readout_workspace_size",
                           "solo_readout_kernel_family", "solo_readout_fwd_bwd", "solo_readout_fwd_bwd_profiled",
                           "solo_readout_general_workspace_size", "solo_readout_general",
-                          "solo_readout_exit_eval_workspace_size", "solo_readout_exit_eval"}
+                          "solo_readout_exit_eval_workspace_size", "solo_readout_exit_eval",
+                          "solo_readout_scratch_limit", "solo_readout_fwd_bwd_noalloc"}
     lib = ctypes.CDLL(LIB)
     for n in names:
         assert hasattr(lib, n), n
@@ -261,3 +262,23 @@ def test_general_null_args_pointer():
 def test_exit_eval_validation_errors(kw, code):
     # exit evaluation needs no gradient outputs: dh, dW, dgain may be NULL
     assert B.exit_eval_raw(gargs(dh=0, dW=0, dgain=0, **kw)) == B.STATUS[code]
+
+
+def test_noalloc_entry_point_validates_on_the_host():
+    # argument errors and calls beyond the static scratch are refused before any HIP call
+    assert B.scratch_limit() == 128 << 20
+    def na(**kw):
+        a = dict(K=2, T=8, d=64, V=32, dtype=B.SOLO_BF16, eps=1e-6, h=P, gain=P, W=P, targets=P, final_module_dW=1,
+                 losses=P, row_loss=0, dh=P, dW=P, dgain=P, stream=0)
+        a.update(kw)
+        return B.readout_fwd_bwd_noalloc_raw(**a)
+    assert na(dtype=5) == B.STATUS["SOLO_ERR_DTYPE"]
+    assert na(K=0) == B.STATUS["SOLO_ERR_SHAPE"]
+    assert na(d=60) == B.STATUS["SOLO_ERR_SHAPE"]
+    assert na(h=0) == B.STATUS["SOLO_ERR_NULL"]
+    assert na(dW=0) == B.STATUS["SOLO_ERR_NULL"]
+    assert na(dh=P + 2) == B.STATUS["SOLO_ERR_ALIGN"]
+    assert na(eps=-1.0) == B.STATUS["SOLO_ERR_ARG"]
+    big = dict(K=4, T=65536, d=2048, V=32000)
+    assert B.workspace_size(big["K"], big["T"], big["d"], big["V"], B.SOLO_BF16, True) > B.scratch_limit()
+    assert na(**big) == B.STATUS["SOLO_ERR_WORKSPACE"]
