@@ -46,6 +46,9 @@ VARIANTS = {
     "priv": (dict(wbar="per_head", tau=True, bias=True),
              dict(final_module_dW=True, heads_train_readout=True, want_dtau=True, want_dbias=True),
              "one trained readout per head (PRIV): every module's readout gradient"),
+    "rot": (dict(rot=True, tau=True, bias=True),
+            dict(final_module_dW=True, want_dtau=True, want_dbias=True),
+            "the shared readout in a fixed orthogonal basis per head (ROT, Wbar R_k), temperatures and biases"),
     "exit_eval": (dict(), None, "forward-only exit evaluation: losses and top-1 of every exit"),
 }
 
@@ -122,7 +125,12 @@ def cpu_baseline(cfg_name: str, sample_T: int, seed: int = 0, variant: str = "he
         from solo_inputs import make_extras
 
         e = make_extras(x, seed, **extras)
-        kw = dict(Wbar=e.get("Wbar"), tau=e.get("tau"), bias=e.get("bias"))
+        Wbar = e.get("Wbar")
+        if e.get("rot") is not None:
+            # the oracle reads ROT heads as one readout each, Wbar R_k (formed before the clock starts)
+            base = W if Wbar is None else Wbar.astype(np.float64)
+            Wbar = np.stack([base @ r.astype(np.float64) for r in e["rot"]])
+        kw = dict(Wbar=Wbar, tau=e.get("tau"), bias=e.get("bias"))
         t0 = time.perf_counter()
         if flags is None:
             oracle.exit_eval(h, e["gain"], W, x["targets"], **kw)
@@ -241,7 +249,7 @@ def main(argv=None) -> int:
         elem = 4
     targets = torch.from_numpy(x["targets"]).to(dev)
     extras, flags, vdesc = VARIANTS[args.variant]
-    Wbar = tau = bias = None
+    Wbar = tau = bias = rot = None
     if extras is not None:
         from solo_inputs import make_extras
 
@@ -258,6 +266,7 @@ def main(argv=None) -> int:
 
         gain = up_any("gain")
         Wbar = up_any("Wbar")
+        rot = up_any("rot")
         tau = torch.from_numpy(e["tau"]).to(dev) if e.get("tau") is not None else None
         bias = torch.from_numpy(e["bias"]).to(dev) if e.get("bias") is not None else None
         del e
@@ -282,12 +291,13 @@ def main(argv=None) -> int:
         del out
         # first call sizes and allocates the workspace and outputs; the timed calls reuse them
         if flags is None:
-            r = binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, stream=stream)
+            r = binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, rot=rot, stream=stream)
         else:
-            r = binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, stream=stream, **flags)
+            r = binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, rot=rot, stream=stream,
+                                        **flags)
         gout[0] = r
         torch.cuda.synchronize()
-        a = binding._fill_inputs(h, gain, W, targets, Wbar, tau, bias, 1e-6)[0]
+        a = binding._fill_inputs(h, gain, W, targets, Wbar, tau, bias, 1e-6, rot)[0]
         if flags is None:
             nbytes = binding.exit_eval_workspace_size(a)
         else:
@@ -307,11 +317,11 @@ def main(argv=None) -> int:
             binding.readout_fwd_bwd(h, gain, W, targets, True, 1e-6, workspace=ws, out=out, stream=stream,
                                     stage_events=stage)
         elif flags is None:
-            binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, workspace=ws, stream=stream,
-                              stage_events=stage, out=gout[0])
+            binding.exit_eval(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, rot=rot, workspace=ws,
+                              stream=stream, stage_events=stage, out=gout[0])
         else:
-            binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, workspace=ws, stream=stream,
-                                    stage_events=stage, out=gout[0], **flags)
+            binding.readout_general(h, gain, W, targets, Wbar=Wbar, tau=tau, bias=bias, rot=rot, workspace=ws,
+                                    stream=stream, stage_events=stage, out=gout[0], **flags)
 
     for _ in range(args.warmup):
         step()
@@ -352,7 +362,8 @@ def main(argv=None) -> int:
                                         heads_train_readout=fl.get("heads_train_readout", False), exit_eval=is_eval)
     exe_flops = costmodel.executed_flops(K, T, V, d, final_module_dW=fl.get("final_module_dW", True),
                                          heads_train_readout=fl.get("heads_train_readout", False),
-                                         bias_grad=fl.get("want_dbias", False), exit_eval=is_eval)
+                                         bias_grad=fl.get("want_dbias", False), exit_eval=is_eval,
+                                         rot=rot is not None)
     tokens_per_s = T / (ms_per_step / 1e3)
     # dominant kernel: the local-loss pass, 2r per token of every module (logits + input
     # gradient), or the exit evaluation's forward pass (1r)

@@ -30,9 +30,10 @@
  * (phi_k, tau_k, b_k), the terminal trains (W, b)), a gain g_k per module or
  * one shared gain, and the heads' readout R_k (k < K-1) taken from W itself
  * (SOLO), one other matrix shared by the heads (SOLO's copy from an earlier
- * step when it is refreshed every S > 1 steps; RSHARE), or one matrix per
- * head (RAND frozen, PRIV trained, ROT the caller's W R_k).  The terminal
- * always reads W.  solo_readout_exit_eval is the forward pass alone: every
+ * step when it is refreshed every S > 1 steps; RSHARE), one matrix per head
+ * (RAND frozen, PRIV trained), or the shared matrix in a fixed orthogonal
+ * basis per head, Wbar R_k (ROT: same content and range, another basis;
+ * Appendix D).  The terminal always reads W.  solo_readout_exit_eval is the forward pass alone: every
  * exit's loss and top-1 prediction through its readout (early exit through
  * the shared readout, Section 4).
  *
@@ -49,7 +50,7 @@
 extern "C" {
 #endif
 
-#define SOLO_READOUT_ABI_VERSION 2
+#define SOLO_READOUT_ABI_VERSION 3
 
 /* Element type of h, gain, W, Wbar and dh.  Statistics, exponentials and
  * accumulation are fp32 in both cases; the bf16 path multiplies bf16
@@ -79,11 +80,13 @@ const char* solo_status_string(int status);
 
 /*
  * Bytes of device workspace one solo_readout_fwd_bwd call needs.  A function
- * of (K, T, d, V, dtype, final_module_dW) with no T*V and no V*d term: per-token
+ * of (K, T, d, V, dtype, final_module_dW) with no T*V term: per-token
  * statistics, per-tile partial sums of the gain gradient and, on the
- * matrix-core family, a bf16 copy of gain * h of the modules whose readout or
- * bias gradient is computed (T*d*2 bytes each).  Returns 0 for arguments that
- * solo_readout_fwd_bwd would reject.
+ * matrix-core families, a bf16 copy of gain * h of the modules whose readout or
+ * bias gradient is computed (T*d*2 bytes each, rounded up to 16 rows); on the
+ * "mfma_wide" family also one tiled bf16 copy of W (V*d*2 bytes, V rounded up
+ * to 16), and the same for each distinct heads' readout of the general
+ * entry point.  Returns 0 for arguments that solo_readout_fwd_bwd would reject.
  */
 size_t solo_readout_workspace_size(int K, int T, int d, int V, int dtype, int final_module_dW);
 
@@ -221,6 +224,18 @@ int solo_readout_fwd_bwd_noalloc(int K, int T, int d, int V, int dtype, float ep
  *                   has none, so pass tau[K-1] = 1 for that).  Not checked for
  *                   finiteness.  4-byte aligned.
  *   bias            [K][V] float or NULL (no bias).  4-byte aligned.
+ *   rot             [K-1][d][d] dtype or NULL, 16-byte aligned (ROT): head k
+ *                   reads Wbar R_k (Wbar = W when Wbar is NULL; needs
+ *                   readout_per_head = 0), i.e. z_tv = tau_k <Wbar_v, R_k hhat_t>
+ *                   + b_kv.  R_k is used as given (orthogonality is not
+ *                   checked).  The library rotates the heads' normalised
+ *                   rows instead of forming Wbar R_k: u_t = R_k (g_k * h_t)
+ *                   (rounded to bf16 on the bf16 path, as the product
+ *                   g_k * h_t is there) and, backward, R_k^T applied to
+ *                   sum_v delta_tv Wbar_v (2 T d^2 multiply-adds per head each
+ *                   way).  The workspace then also holds (K-1) T d elements of
+ *                   u and, for fwd_bwd, 2 (K-1) T d floats and (K-1) d^2
+ *                   elements.  Ignored when K = 1.
  *
  * Which gradients (fwd_bwd only; exit evaluation computes none):
  *   final_module_dW      dW of the terminal, and with a shared gain its dgain.
@@ -249,7 +264,11 @@ int solo_readout_fwd_bwd_noalloc(int K, int T, int d, int V, int dtype, float ep
  *
  * Semantics and errors as for solo_readout_fwd_bwd.  SOLO_ERR_ARG also for:
  * a flag not 0 or 1, readout_per_head without Wbar, heads_train_readout
- * without readout_per_head.
+ * without readout_per_head, rot with readout_per_head.
+ *
+ * ABI version 3 appended rot to the end of the struct (a caller built against
+ * version 2 that zero-fills a version-2 struct must not pass it to a
+ * version-3 library: the library reads the new field).
  */
 typedef struct solo_readout_args {
     int K, T, d, V;
@@ -279,6 +298,7 @@ typedef struct solo_readout_args {
     size_t workspace_bytes;
     void* hip_stream;
     void* const* stage_events;
+    const void* rot;
 } solo_readout_args;
 
 /* Workspace bytes of solo_readout_general with these arguments (only the
@@ -289,7 +309,9 @@ size_t solo_readout_general_workspace_size(const solo_readout_args* args);
 /* Forward and local backward with every option above. */
 int solo_readout_general(const solo_readout_args* args);
 
-/* Workspace bytes of solo_readout_exit_eval (a function of K and T). */
+/* Workspace bytes of solo_readout_exit_eval: per-token statistics (K T
+ * floats each), the tiled readout copies of the matrix-core families (V d
+ * terms, as for the general entry point) and, with rot, the rotated rows. */
 size_t solo_readout_exit_eval_workspace_size(const solo_readout_args* args);
 
 /* Forward-only exit evaluation: losses, row_loss and top1 of every module. */

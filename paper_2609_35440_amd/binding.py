@@ -76,6 +76,7 @@ class SoloReadoutArgs(ctypes.Structure):
         ("dtau", ctypes.c_void_p), ("dbias", ctypes.c_void_p), ("top1", ctypes.c_void_p),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
         ("hip_stream", ctypes.c_void_p), ("stage_events", ctypes.c_void_p),
+        ("rot", ctypes.c_void_p),
     ]
 
 
@@ -363,7 +364,7 @@ def _ptr(t):
     return t.data_ptr() if t is not None else None
 
 
-def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps):
+def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps, rot=None):
     """Validate shapes and build the input part of SoloReadoutArgs (tensors kept alive by the caller)."""
     import torch
 
@@ -381,45 +382,54 @@ def _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps):
         raise ValueError("tau must be [K]")
     if bias is not None and tuple(bias.shape) != (K, V):
         raise ValueError("bias must be [K,V]")
-    dts = {h.dtype, gain.dtype, W.dtype} | ({Wbar.dtype} if Wbar is not None else set())
+    if rot is not None:
+        if tuple(rot.shape) != (K - 1, d, d):
+            raise ValueError(f"rot must be [K-1,d,d], got {tuple(rot.shape)}")
+        if Wbar is not None and Wbar.dim() == 3:
+            raise ValueError("rot rotates one shared readout: Wbar must be None or [V,d]")
+    dts = {h.dtype, gain.dtype, W.dtype} | ({Wbar.dtype} if Wbar is not None else set()) \
+        | ({rot.dtype} if rot is not None else set())
     if len(dts) != 1:
-        raise TypeError("h, gain, W and Wbar must share one dtype")
-    for t in (h, gain, W, targets, Wbar, tau, bias):
+        raise TypeError("h, gain, W, Wbar and rot must share one dtype")
+    for t in (h, gain, W, targets, Wbar, tau, bias, rot):
         if t is not None and not t.is_cuda:
             raise ValueError("all inputs must be GPU tensors")
     _check_targets(targets)
-    _check_device(h.device, {"gain": gain, "W": W, "targets": targets, "Wbar": Wbar, "tau": tau, "bias": bias})
+    _check_device(h.device, {"gain": gain, "W": W, "targets": targets, "Wbar": Wbar, "tau": tau, "bias": bias,
+                             "rot": rot})
     keep = {
         "h": h.contiguous(), "gain": gain.contiguous(), "W": W.contiguous(),
         "Wbar": Wbar.contiguous() if Wbar is not None else None,
         "tau": tau.to(torch.float32).contiguous() if tau is not None else None,
         "bias": bias.to(torch.float32).contiguous() if bias is not None else None,
         "targets": targets.to(torch.int32).contiguous(),
+        "rot": rot.contiguous() if rot is not None else None,
     }
     a = SoloReadoutArgs()
     a.K, a.T, a.d, a.V = K, T, d, V
     a.dtype = _dtype_code(h.dtype)
     a.eps = float(eps)
-    for name in ("h", "gain", "W", "Wbar", "tau", "bias", "targets"):
+    for name in ("h", "gain", "W", "Wbar", "tau", "bias", "targets", "rot"):
         setattr(a, name, _ptr(keep[name]))
     a.gain_per_module = int(gain.dim() == 2)
     a.readout_per_head = int(Wbar is not None and Wbar.dim() == 3)
     return a, keep
 
 
-def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, final_module_dW: bool = True,
+def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, rot=None, final_module_dW: bool = True,
                     heads_train_readout: bool = False, want_dtau: bool = False, want_dbias: bool = False,
                     eps: float = 1e-6, row_loss: bool = False, workspace=None, stream=None,
                     stage_events=None, out: Optional[GeneralResult] = None) -> GeneralResult:
     """The loss with temperatures, biases, per-module gains and readout sources
     (``solo_readout_general``).  ``gain`` [d] or [K, d]; ``Wbar`` None, [V, d] or
-    [K-1, V, d] (same dtype as h); ``tau`` [K] and ``bias`` [K, V] float32 or None.
+    [K-1, V, d] (same dtype as h); ``tau`` [K] and ``bias`` [K, V] float32 or None;
+    ``rot`` [K-1, d, d] (same dtype as h) or None: head k reads (Wbar or W) R_k (ROT).
     Returns GeneralResult; gradients that were not requested are None.  ``out``
     (a GeneralResult from an earlier call with the same arguments) reuses its tensors.
     """
     import torch
 
-    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
+    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps, rot)
     K, T, d, V = a.K, a.T, a.d, a.V
     dev = h.device
     f32 = dict(dtype=torch.float32, device=dev)
@@ -471,14 +481,15 @@ def readout_general(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, fina
     return out
 
 
-def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, eps: float = 1e-6, row_loss: bool = True,
+def exit_eval(h, gain, W, targets, *, Wbar=None, tau=None, bias=None, rot=None, eps: float = 1e-6,
+              row_loss: bool = True,
               top1: bool = True, workspace=None, stream=None, stage_events=None,
               out: Optional[EvalResult] = None) -> EvalResult:
     """Forward-only exit evaluation (``solo_readout_exit_eval``): losses [K],
     row_loss [K, T] and top1 [K, T] int32 (argmax of the logits, lowest index on ties)."""
     import torch
 
-    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps)
+    a, keep = _fill_inputs(h, gain, W, targets, Wbar, tau, bias, eps, rot)
     K, T = a.K, a.T
     dev = h.device
     made = []

@@ -50,20 +50,24 @@ def general_flops(K: int, T: int, V: int, d: int, *, final_module_dW: bool = Tru
 
 
 def executed_flops(K: int, T: int, V: int, d: int, *, final_module_dW: bool = True,
-                   heads_train_readout: bool = False, bias_grad: bool = False, exit_eval: bool = False) -> int:
+                   heads_train_readout: bool = False, bias_grad: bool = False, exit_eval: bool = False,
+                   rot: bool = False) -> int:
     """Matrix-product FLOPs the fused kernels execute for the same call.
 
     Local-loss pass: 2r per module (logits and the input-gradient product).
     Readout-gradient pass: 2r per module in it (the logits again, with the
     stored log-sum-exp, and the weight-gradient product).  Bias-gradient pass
     (modules whose bias but not readout gets a gradient): 1r per module, the
-    logits again.  Exit evaluation: 1r per module.
+    logits again.  Exit evaluation: 1r per module.  ROT (head k reads Wbar R_k)
+    adds the rotation of each head's rows, 2 T d^2, and in the backward pass
+    the rotation of its gradient back, 2 T d^2 more.
     """
+    rotf = (K - 1) * 2 * T * d * d if rot and K > 1 else 0
     if exit_eval:
-        return 2 * K * T * V * d
+        return 2 * K * T * V * d + rotf
     rg = (1 if final_module_dW else 0) + ((K - 1) if heads_train_readout else 0)
     bg = (K - rg) if bias_grad else 0
-    return 2 * (2 * K + 2 * rg + bg) * T * V * d
+    return 2 * (2 * K + 2 * rg + bg) * T * V * d + 2 * rotf
 
 
 def readout_bytes(K: int, T: int, V: int, d: int, elem_bytes: int = 2, final_module_dW: bool = True) -> int:

@@ -108,8 +108,8 @@ __device__ __forceinline__ const bf16* tiled_readout_of(const FusedArgs& a, int 
     return k == a.K - 1 ? (const bf16*)a.Wtt : (const bf16*)a.Wht + (long long)k * a.wht_stride;
 }
 
-// MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
-// MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
+// MODE LOCAL / EVAL: grid (ceil(T/XR), nmod); MODE RGRAD / BGRAD: grid
+// (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
 // EXT (LOCAL and EVAL): the variant with per-chunk biases, launched when the call has biases.
 template <int MODE, int DS, bool EXT>
 __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
     const int d = a.d;
     const int js = w * DS;
     const int x0 = blockIdx.x * XR;
-    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
+    const int k = a.m0 + (int)blockIdx.y;
     const long long modoff = (long long)k * a.T;
     const float tau_k = a.tau ? a.tau[k] : 1.f;
 
@@ -596,6 +596,20 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             for (int ww = 0; ww < NW; ++ww) csum += cbuf[ww * XR + 32 * h + ex];
             const float cmean = tau_k * csum / (float)d;
             if (a.rowdtau && w == 0 && ehh == 0 && xok[h]) a.rowdtau[modoff + xg] = tok[h] ? csum : 0.f;
+            if (a.ebuf) {
+                // e to the buffer; the RMSNorm backward follows the rotation back
+                if (xok[h]) {
+#pragma unroll
+                    for (int b = 0; b < (PC ? G::NB : 1); ++b)
+#pragma unroll
+                        for (int i4 = 0; i4 < 4; ++i4) {
+                            const f32x4 o = {acc[b][h][4 * i4], acc[b][h][4 * i4 + 1], acc[b][h][4 * i4 + 2],
+                                             acc[b][h][4 * i4 + 3]};
+                            *(f32x4*)(a.ebuf + (modoff + xg) * (long long)d + js + 32 * b + 8 * i4 + 4 * ehh) = o;
+                        }
+                }
+                continue;
+            }
             LDS_AS char* srow = (ex < 16 ? sliceA : sliceB) + (ex & 15) * (2 * DS);
 #pragma unroll
             for (int b = 0; b < (PC ? G::NB : 1); ++b) {
@@ -627,7 +641,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
         // sweep 3, for a module that trains its gain: the tile's partial sums
         // of dhhat * n = tau e * n over its rows (the 16-lane row, the other row
         // of the half-wave, then the other 32-row half of the tile)
-        if (want_dg) {
+        if (want_dg && !a.ebuf) {
 #pragma unroll
             for (int b = 0; b < (PC ? G::NB : 1); ++b) {
 #pragma unroll
@@ -684,7 +698,7 @@ template <int MODE, int DS, bool EXT>
 hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
     const bool ll = MODE == LOCAL || MODE == EVAL;
     constexpr int XR = Geo<DS, MODE == LOCAL || MODE == RGRAD>::XR;
-    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
+    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)nmod)
                    : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
     return hipGetLastError();
@@ -711,11 +725,11 @@ bool mfma_supported(int dtype, int d) { return dtype == 0 && d % (NW * 32) == 0 
 
 int mfma_rows(int d) { return d <= NW * 128 ? rows_of<128, true>() : rows_of<256, true>(); }
 
-hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s) {
-    return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
+hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, int nmod, hipStream_t s) {
+    return ext ? launch_mode<LOCAL, true>(a, nmod, s) : launch_mode<LOCAL, false>(a, nmod, s);
 }
-hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s) {
-    return a.bias ? launch_mode<EVAL, true>(a, 0, s) : launch_mode<EVAL, false>(a, 0, s);
+hipError_t launch_exit_eval_mfma(const FusedArgs& a, int nmod, hipStream_t s) {
+    return a.bias ? launch_mode<EVAL, true>(a, nmod, s) : launch_mode<EVAL, false>(a, nmod, s);
 }
 hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s) {
     return launch_mode<RGRAD, false>(a, nmod, s);

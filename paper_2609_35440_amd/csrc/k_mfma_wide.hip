@@ -72,8 +72,8 @@ __device__ __forceinline__ const bf16* readout_of(const FusedArgs& a, int k) {
     return k == a.K - 1 ? (const bf16*)a.Wt : (const bf16*)a.Wh + (long long)k * a.wh_stride;
 }
 
-// MODE LOCAL / EVAL: grid (ceil(T/XR), K); module k = blockIdx.y.
-// MODE RGRAD / BGRAD: grid (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
+// MODE LOCAL / EVAL: grid (ceil(T/XR), nmod); MODE RGRAD / BGRAD: grid
+// (ceil(V/XR), nmod); module k = m0 + blockIdx.y.
 // XR = 16 with a second product (LOCAL, RGRAD), 48 without (EVAL, BGRAD).
 // EXT (LOCAL and EVAL): the variant with per-chunk biases, launched when the call has biases.
 template <int MODE, int DS, bool EXT>
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
     const int d = a.d;
     const int js = w * DS;
     const int x0 = blockIdx.x * XR;
-    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
+    const int k = a.m0 + (int)blockIdx.y;
     const long long modoff = (long long)k * a.T;
     const float tau_k = a.tau ? a.tau[k] : 1.f;
 
@@ -431,8 +431,14 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         const float cmean = tau_k * csum / (float)d;
         if (a.rowdtau && w == 0 && eg == 0 && xok) a.rowdtau[modoff + xg] = tok ? csum : 0.f;
 
-        // sweep 2: dh = r (dn - c n)
-        if (xok) {
+        // sweep 2: dh = r (dn - c n); or e to the buffer, whose RMSNorm backward
+        // follows the rotation back (ROT heads)
+        if (xok && a.ebuf) {
+#pragma unroll
+            for (int b = 0; b < G::NB; ++b)
+                *(f32x4*)(a.ebuf + (modoff + xg) * (long long)d + js + 16 * b + 4 * eg) = acc[b];
+        }
+        if (xok && !a.ebuf) {
             bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;
 #pragma unroll
             for (int b = 0; b < G::NB; ++b) {
@@ -450,7 +456,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         }
         // sweep 3, for a module that trains its gain: the tile's partial sums
         // of dhhat * n = tau e * n over its 16 rows
-        if (want_dg) {
+        if (want_dg && !a.ebuf) {
 #pragma unroll
             for (int b = 0; b < G::NB; ++b) {
                 const int j = js + 16 * b + 4 * eg;
@@ -486,7 +492,7 @@ template <int MODE, int DS, bool EXT>
 hipError_t launch_ds(const FusedArgs& a, int nmod, hipStream_t s) {
     const bool ll = MODE == LOCAL || MODE == EVAL;
     constexpr int XR = wide_rows<MODE == LOCAL || MODE == RGRAD>();
-    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)a.K)
+    dim3 grid = ll ? dim3((unsigned)((a.T + XR - 1) / XR), (unsigned)nmod)
                    : dim3((unsigned)((a.V + XR - 1) / XR), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused_wide<MODE, DS, EXT>), grid, dim3(NTHR), 0, s, a);
     return hipGetLastError();
@@ -504,11 +510,11 @@ hipError_t launch_mode(const FusedArgs& a, int nmod, hipStream_t s) {
 
 bool mfma_wide_supported(int dtype, int d) { return dtype == 0 && d == 2560; }
 
-hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, hipStream_t s) {
-    return ext ? launch_mode<LOCAL, true>(a, 0, s) : launch_mode<LOCAL, false>(a, 0, s);
+hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, int nmod, hipStream_t s) {
+    return ext ? launch_mode<LOCAL, true>(a, nmod, s) : launch_mode<LOCAL, false>(a, nmod, s);
 }
-hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s) {
-    return a.bias ? launch_mode<EVAL, true>(a, 0, s) : launch_mode<EVAL, false>(a, 0, s);
+hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s) {
+    return a.bias ? launch_mode<EVAL, true>(a, nmod, s) : launch_mode<EVAL, false>(a, nmod, s);
 }
 hipError_t launch_readout_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s) {
     return launch_mode<RGRAD, false>(a, nmod, s);

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
     const int lane = tid & 63;
     const int wv = tid >> 6;
     const int x0 = blockIdx.x * RX;
-    const int k = LL ? (int)blockIdx.y : a.m0 + (int)blockIdx.y;
+    const int k = a.m0 + (int)blockIdx.y;
     const long long modoff = (long long)k * a.T;
     const float tau = a.tau ? a.tau[k] : 1.f;
     const E* hk = (const E*)a.h + modoff * d;
@@ -258,7 +258,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
                     const float ev = fmaf(acc[r][q], sc[r], spy[r] * wy) * a.inv_T;
                     const float n = (xg < nX) ? rx * ld(hk, (long long)xg * d + j) : 0.f;
                     const float gj = ld(gk, j);
-                    acc[r][q] = tau * gj * ev;          // dn
+                    acc[r][q] = a.ebuf ? ev : tau * gj * ev;  // dn (e itself for the buffer)
                     cp[r] = fmaf(gj * ev, n, cp[r]);
                     dgp[q] = fmaf(tau * ev, n, dgp[q]);
                 }
@@ -286,6 +286,15 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
             if (a.rowdtau && tid == 0) {
                 const int tg = a.targets[modoff + xg];
                 a.rowdtau[modoff + xg] = (tg >= 0 && tg < nY) ? csum : 0.f;
+            }
+            if (a.ebuf) {
+                // e to the buffer; the RMSNorm backward follows the rotation back (ROT heads)
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    const int j = tid + NTHR * q;
+                    if (j < d) a.ebuf[(modoff + xg) * (long long)d + j] = acc[r][q];
+                }
+                continue;
             }
             const float rx = a.rstd[modoff + xg];
             E* out = (E*)a.dh + (modoff + xg) * (long long)d;
@@ -324,7 +333,7 @@ hipError_t launch_t(const FusedArgs& a, int nmod, hipStream_t s) {
                                        (int)lds);
     if (e != hipSuccess) return e;
     const bool ll = MODE == LOCAL || MODE == EVAL;
-    dim3 grid = ll ? dim3((unsigned)((a.T + RX - 1) / RX), (unsigned)a.K)
+    dim3 grid = ll ? dim3((unsigned)((a.T + RX - 1) / RX), (unsigned)nmod)
                    : dim3((unsigned)((a.V + RX - 1) / RX), (unsigned)nmod);
     hipLaunchKernelGGL((k_fused_valu<E, MODE>), grid, dim3(NTHR), lds, s, a);
     return hipGetLastError();
@@ -337,8 +346,12 @@ hipError_t launch_dt(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s) { return launch_dt<LOCAL>(dtype, a, 0, s); }
-hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, hipStream_t s) { return launch_dt<EVAL>(dtype, a, 0, s); }
+hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_dt<LOCAL>(dtype, a, nmod, s);
+}
+hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
+    return launch_dt<EVAL>(dtype, a, nmod, s);
+}
 hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s) {
     return launch_dt<RGRAD>(dtype, a, nmod, s);
 }

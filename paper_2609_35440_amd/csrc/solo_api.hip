@@ -36,8 +36,13 @@ struct Plan {
     int bg_lo = 0, bg_hi = 0;  // modules of the bias-gradient pass
     int hg_lo = 0, hg_hi = 0;  // modules whose gain-scaled copy the matrix-core gradient passes stream
     int nhead_tiles = 0;       // tiled copies of the heads' readouts (0: the heads read W's copy)
+    int rows = 0;              // token rows per tile of the local-loss pass
+    bool rot = false;          // ROT heads: modules 0..K-2 read Wbar R_k through rotated rows
     size_t rstd = 0, lse = 0, rowloss = 0, rowrec = 0, rowdtau = 0, dgp = 0, hg = 0;
     size_t wtile = 0, whtile = 0, total = 0;
+    // ROT pieces: a vector of ones (the rotated rows' gain), the rotated rows
+    // u, the heads' e = sum_v delta_v Wbar_v (fp32), D = e R_k (fp32), R_k^T
+    size_t ones = 0, ubuf = 0, ebuf = 0, dbuf = 0, rtr = 0;
 };
 
 // Which passes stream tiled copies: every pass of the wide tiling; in the
@@ -54,6 +59,7 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
     if (!flag_ok(a.gain_per_module) || !flag_ok(a.readout_per_head) || !flag_ok(a.final_module_dW) ||
         !flag_ok(a.heads_train_readout))
         return false;
+    if (a.rot && a.readout_per_head) return false;
     const int K = a.K, T = a.T, d = a.d;
     P->wide = solo::mfma_wide_supported(a.dtype, d);
     P->mfma = solo::mfma_supported(a.dtype, d) || P->wide;
@@ -75,6 +81,26 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
         off = align_up(off + tv);
         P->whtile = off;
         off = align_up(off + tv * P->nhead_tiles);
+    }
+    const int rows = P->wide ? solo::kMfmaWideRows : (P->mfma ? solo::mfma_rows(d) : solo::kValuRows);
+    P->rows = rows;
+    P->ntiles = (T + rows - 1) / rows;
+    P->rot = a.rot != nullptr && K > 1;
+    if (P->rot) {
+        const size_t es = a.dtype == SOLO_BF16 ? 2 : 4;
+        const size_t htd = (size_t)(K - 1) * T * d;
+        P->ones = off;
+        off = align_up(off + (size_t)d * es);
+        P->ubuf = off;
+        off = align_up(off + htd * es);
+        if (!eval) {
+            P->ebuf = off;
+            off = align_up(off + htd * 4);
+            P->dbuf = off;
+            off = align_up(off + htd * 4);
+            P->rtr = off;
+            off = align_up(off + (size_t)(K - 1) * d * d * es);
+        }
     }
     if (eval) {
         P->total = off;
@@ -104,8 +130,6 @@ bool make_plan(const solo_readout_args& a, bool eval, Plan* P) {
     P->ext = a.bias != nullptr;
     P->dg_mode = a.gain_per_module ? 2 : (fdw ? 1 : 0);
     P->slots = P->dg_mode == 2 ? K : (P->dg_mode == 1 ? 1 : 0);
-    const int rows = P->wide ? solo::kMfmaWideRows : (P->mfma ? solo::mfma_rows(d) : solo::kValuRows);
-    P->ntiles = (T + rows - 1) / rows;
     const bool second = P->rg_hi > P->rg_lo || P->bg_hi > P->bg_lo;
     if (P->mfma && second) {
         // the two ranges are disjoint parts of [0, K): their union is one range
@@ -137,6 +161,7 @@ int check(const solo_readout_args& a, bool eval, Plan* P) {
         return SOLO_ERR_ARG;
     if (a.readout_per_head && !a.Wbar) return SOLO_ERR_ARG;
     if (a.heads_train_readout && !a.readout_per_head) return SOLO_ERR_ARG;
+    if (a.rot && a.readout_per_head) return SOLO_ERR_ARG;
     if (!a.h || !a.gain || !a.W || !a.targets || !a.losses || !a.workspace) return SOLO_ERR_NULL;
     if (!eval) {
         if (!a.dh) return SOLO_ERR_NULL;
@@ -146,7 +171,8 @@ int check(const solo_readout_args& a, bool eval, Plan* P) {
     }
     if (!aligned(a.h, 16) || !aligned(a.gain, 16) || !aligned(a.W, 16) || !aligned_or_null(a.Wbar, 16) ||
         !aligned(a.targets, 4) || !aligned(a.losses, 4) || !aligned_or_null(a.row_loss, 4) ||
-        !aligned_or_null(a.tau, 4) || !aligned_or_null(a.bias, 4) || !aligned(a.workspace, kAlign))
+        !aligned_or_null(a.tau, 4) || !aligned_or_null(a.bias, 4) || !aligned_or_null(a.rot, 16) ||
+        !aligned(a.workspace, kAlign))
         return SOLO_ERR_ALIGN;
     if (eval) {
         if (!aligned_or_null(a.top1, 4)) return SOLO_ERR_ALIGN;
@@ -222,52 +248,88 @@ int run(const solo_readout_args& x, bool eval) {
                                                (solo::bf16*)(ws + P.whtile), P.nhead_tiles, V, d, s) != hipSuccess)
             return SOLO_ERR_HIP;
     }
+    // ROT heads: their stationary rows are u = R_k (g_k * h) (gain one from
+    // then on), which the passes of the heads read in place of h
+    solo::FusedArgs ah = a;
+    if (P.rot) {
+        if (solo::launch_fill_one(dt, ws + P.ones, d, s) != hipSuccess) return SOLO_ERR_HIP;
+        if (solo::launch_rot_gemm(dt, false, x.h, (long long)T * d, x.gain, a.g_stride, x.rot, (long long)d * d,
+                                  ws + P.ubuf, false, (long long)T * d, K - 1, T, d, d, s) != hipSuccess)
+            return SOLO_ERR_HIP;
+        ah.h = ws + P.ubuf;
+        ah.gain = ws + P.ones;
+        ah.g_stride = 0;
+        ah.ebuf = eval ? nullptr : (float*)(ws + P.ebuf);
+    }
     if (!mark(0)) return SOLO_ERR_HIP;
-    hipError_t e;
-    if (eval)
-        e = P.wide   ? solo::launch_exit_eval_mfma_wide(a, s)
-            : P.mfma ? solo::launch_exit_eval_mfma(a, s)
-                     : solo::launch_exit_eval_valu(dt, a, s);
-    else
-        e = P.wide   ? solo::launch_local_loss_mfma_wide(a, P.ext, s)
-            : P.mfma ? solo::launch_local_loss_mfma(a, P.ext, s)
-                     : solo::launch_local_loss_valu(dt, a, s);
-    if (e != hipSuccess || !mark(1)) return SOLO_ERR_HIP;
+    // one launch over modules [m0, m0 + n) of a pass, with the arguments g
+    auto pass = [&](int which, const solo::FusedArgs& g, int m0, int n) -> hipError_t {
+        if (n <= 0) return hipSuccess;
+        solo::FusedArgs b = g;
+        b.m0 = m0;
+        switch (which) {
+            case 0:
+                return P.wide   ? solo::launch_exit_eval_mfma_wide(b, n, s)
+                       : P.mfma ? solo::launch_exit_eval_mfma(b, n, s)
+                                : solo::launch_exit_eval_valu(dt, b, n, s);
+            case 1:
+                return P.wide   ? solo::launch_local_loss_mfma_wide(b, P.ext, n, s)
+                       : P.mfma ? solo::launch_local_loss_mfma(b, P.ext, n, s)
+                                : solo::launch_local_loss_valu(dt, b, n, s);
+            case 2:
+                return P.wide   ? solo::launch_readout_grad_mfma_wide(b, n, s)
+                       : P.mfma ? solo::launch_readout_grad_mfma(b, n, s)
+                                : solo::launch_readout_grad_valu(dt, b, n, s);
+            default:
+                return P.wide   ? solo::launch_bias_grad_mfma_wide(b, n, s)
+                       : P.mfma ? solo::launch_bias_grad_mfma(b, n, s)
+                                : solo::launch_bias_grad_valu(dt, b, n, s);
+        }
+    };
+    // modules [lo, hi) of a pass: under ROT the heads and the terminal are two launches
+    auto pass_range = [&](int which, int lo, int hi) -> bool {
+        if (!P.rot || hi <= K - 1 || lo >= K - 1) return pass(which, P.rot && lo < K - 1 ? ah : a, lo, hi - lo) == hipSuccess;
+        return pass(which, ah, lo, K - 1 - lo) == hipSuccess && pass(which, a, K - 1, hi - K + 1) == hipSuccess;
+    };
+    if (!pass_range(eval ? 0 : 1, 0, K)) return SOLO_ERR_HIP;
+    if (P.rot && !eval) {
+        // back to the basis of h: D = e R_k = e (R_k^T)^T, then the heads' RMSNorm
+        // backward (and their gain partials when every module trains its gain)
+        if (solo::launch_transpose(dt, x.rot, ws + P.rtr, K - 1, d, s) != hipSuccess ||
+            solo::launch_rot_gemm(dt, true, ws + P.ebuf, (long long)T * d, nullptr, 0, ws + P.rtr, (long long)d * d,
+                                  ws + P.dbuf, true, (long long)T * d, K - 1, T, d, d, s) != hipSuccess ||
+            solo::launch_rot_post(dt, (const float*)(ws + P.dbuf), x.h, x.gain, a.g_stride, (const float*)(ws + P.rstd),
+                                  x.tau, x.dh, P.dg_mode == 2 ? a.dgain_part : nullptr, K - 1, T, d, P.rows,
+                                  s) != hipSuccess)
+            return SOLO_ERR_HIP;
+    }
+    if (!mark(1)) return SOLO_ERR_HIP;
     if (solo::launch_module_sum(a.rowloss, x.losses, K, T, 1.0 / (double)T, s) != hipSuccess) return SOLO_ERR_HIP;
     if (a.rowdtau && solo::launch_module_sum(a.rowdtau, x.dtau, K, T, 1.0, s) != hipSuccess) return SOLO_ERR_HIP;
     if (!mark(2)) return SOLO_ERR_HIP;
     // the gain-scaled copies of h the gradient passes stream, module m at
     // hg + (m - hg_lo) tiled_elems(T, d): tiled for the register-fed passes,
     // row-major for the direct-to-LDS readout-gradient pass
-    auto gain_copies = [&](int lo, int hi, bool as_tiles) -> bool {
+    // (ROT heads: of their rotated rows, times the gain of ones)
+    auto copies = [&](const solo::FusedArgs& g, int lo, int hi, bool as_tiles) -> bool {
         if (hi <= lo) return true;
-        const solo::bf16* src = (const solo::bf16*)x.h + (long long)lo * T * d;
-        const solo::bf16* g = (const solo::bf16*)x.gain + (long long)lo * a.g_stride;
+        const solo::bf16* src = (const solo::bf16*)g.h + (long long)lo * T * d;
+        const solo::bf16* gn = (const solo::bf16*)g.gain + (long long)lo * g.g_stride;
         solo::bf16* dst = (solo::bf16*)(ws + P.hg) + (long long)(lo - P.hg_lo) * solo::tiled_elems(T, d);
-        return (as_tiles ? solo::launch_tile(src, (long long)T * d, g, a.g_stride, dst, hi - lo, T, d, s)
-                         : solo::launch_gain_rows(src, (long long)T * d, g, a.g_stride, dst, solo::tiled_elems(T, d),
-                                                  hi - lo, T, d, s)) == hipSuccess;
+        return (as_tiles ? solo::launch_tile(src, (long long)T * d, gn, g.g_stride, dst, hi - lo, T, d, s)
+                         : solo::launch_gain_rows(src, (long long)T * d, gn, g.g_stride, dst,
+                                                  solo::tiled_elems(T, d), hi - lo, T, d, s)) == hipSuccess;
+    };
+    auto gain_copies = [&](int lo, int hi, bool as_tiles) -> bool {
+        if (!P.rot || hi <= K - 1 || lo >= K - 1) return copies(P.rot && lo < K - 1 ? ah : a, lo, hi, as_tiles);
+        return copies(ah, lo, K - 1, as_tiles) && copies(a, K - 1, hi, as_tiles);
     };
     if (!eval && P.mfma &&
         (!gain_copies(P.rg_lo, P.rg_hi, tiled_rgrad(P)) || !gain_copies(P.bg_lo, P.bg_hi, true)))
         return SOLO_ERR_HIP;
-    if (!eval && P.rg_hi > P.rg_lo) {
-        a.m0 = P.rg_lo;
-        const int n = P.rg_hi - P.rg_lo;
-        e = P.wide   ? solo::launch_readout_grad_mfma_wide(a, n, s)
-            : P.mfma ? solo::launch_readout_grad_mfma(a, n, s)
-                     : solo::launch_readout_grad_valu(dt, a, n, s);
-        if (e != hipSuccess) return SOLO_ERR_HIP;
-    }
+    if (!eval && !pass_range(2, P.rg_lo, P.rg_hi)) return SOLO_ERR_HIP;
     if (!mark(3)) return SOLO_ERR_HIP;
-    if (!eval && P.bg_hi > P.bg_lo) {
-        a.m0 = P.bg_lo;
-        const int n = P.bg_hi - P.bg_lo;
-        e = P.wide   ? solo::launch_bias_grad_mfma_wide(a, n, s)
-            : P.mfma ? solo::launch_bias_grad_mfma(a, n, s)
-                     : solo::launch_bias_grad_valu(dt, a, n, s);
-        if (e != hipSuccess) return SOLO_ERR_HIP;
-    }
+    if (!eval && !pass_range(3, P.bg_lo, P.bg_hi)) return SOLO_ERR_HIP;
     if (!mark(4)) return SOLO_ERR_HIP;
     if (!eval && P.slots) {
         if (solo::launch_dgain_reduce(a.dgain_part, x.dgain, P.slots, P.ntiles, d, s) != hipSuccess)
@@ -372,7 +434,7 @@ const char* solo_status_string(int status) {
         case SOLO_ERR_WORKSPACE: return "workspace too small";
         case SOLO_ERR_ARG:
             return "invalid argument (eps must be finite and >= 0; flags must be 0 or 1; readout_per_head needs "
-                   "Wbar; heads_train_readout needs readout_per_head)";
+                   "Wbar; heads_train_readout needs readout_per_head; rot excludes readout_per_head)";
         case SOLO_ERR_HIP: return "HIP launch failed";
         default: return "unknown status";
     }

@@ -32,7 +32,7 @@ __host__ __device__ inline long long tiled_elems(long long nY, int d) { return (
 // stream Y from its tiled copy (see tiled_elems); the others read Y row-major.
 struct FusedArgs {
     int K, T, d, V;
-    int m0;               // readout-/bias-gradient passes: module of grid row 0 (module = m0 + blockIdx.y)
+    int m0;               // module of grid row 0 (module = m0 + blockIdx.y)
     float inv_T;
     const void* h;        // [K][T][d] elem
     const void* Wt;       // [V][d] elem: readout of module K-1 (the terminal)
@@ -62,6 +62,9 @@ struct FusedArgs {
     float* dWt;           // [V][d] or null: d loss_{K-1} / d W
     float* dWh;           // [K-1][V][d] or null: d loss_k / d readout_k of the heads
     float* dbias;         // [K][V] or null: d loss_k / d b_k
+    float* ebuf;          // [..][T][d] or null: the local-loss pass writes e_t = sum_v delta_tv R_kv (fp32,
+                          // module k at ebuf + k T d) instead of the RMSNorm backward (ROT heads: their
+                          // stationary rows are rotated states, whose gradient is rotated back afterwards)
 };
 
 // Tile sizes of the two kernel families (the workspace depends on them).
@@ -88,18 +91,29 @@ hipError_t launch_dgain_reduce(const float* part, float* dgain, int slots, int n
 // `nmod` is the number of modules of a readout-/bias-gradient launch
 bool mfma_supported(int dtype, int d);
 int mfma_rows(int d);  // stationary rows per workgroup of the matrix-core kernels at width d (64 or 32)
-hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, hipStream_t s);
-hipError_t launch_exit_eval_mfma(const FusedArgs& a, hipStream_t s);
+// local-loss and exit passes: modules m0 .. m0 + nmod - 1
+hipError_t launch_local_loss_mfma(const FusedArgs& a, bool ext, int nmod, hipStream_t s);
+hipError_t launch_exit_eval_mfma(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_readout_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_bias_grad_mfma(const FusedArgs& a, int nmod, hipStream_t s);
 // the wide matrix-core kernels (k_mfma_wide.hip): d = 2560
 bool mfma_wide_supported(int dtype, int d);
-hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, hipStream_t s);
-hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, hipStream_t s);
+hipError_t launch_local_loss_mfma_wide(const FusedArgs& a, bool ext, int nmod, hipStream_t s);
+hipError_t launch_exit_eval_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_readout_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_bias_grad_mfma_wide(const FusedArgs& a, int nmod, hipStream_t s);
-hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, hipStream_t s);
-hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, hipStream_t s);
+hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
+hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
+// ROT (k_rot.hip): C = A B^T per matrix; transposes; a vector of ones; the
+// heads' RMSNorm backward from the rotated-back gradient D = e R_k
+hipError_t launch_rot_gemm(int dtype, bool a_f32, const void* A, long long a_mat, const void* gain, int g_stride,
+                           const void* B, long long b_mat, void* C, bool c_f32, long long c_mat, int nmat, int M,
+                           int N, int Kd, hipStream_t s);
+hipError_t launch_transpose(int dtype, const void* in, void* out, int nmat, int d, hipStream_t s);
+hipError_t launch_fill_one(int dtype, void* p, int n, hipStream_t s);
+hipError_t launch_rot_post(int dtype, const float* D, const void* h, const void* gain, int g_stride,
+                           const float* rstd, const float* tau, void* dh, float* dgain_part, int nmod, int T, int d,
+                           int rows, hipStream_t s);
 hipError_t launch_readout_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
 hipError_t launch_bias_grad_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
 

@@ -27,6 +27,7 @@ __all__ = [
     "zipf_targets",
     "make_inputs",
     "make_extras",
+    "random_orthogonal",
     "make_profile_inputs",
 ]
 
@@ -80,6 +81,7 @@ CONFIGS: Dict[str, Config] = {
 _H, _W, _GAIN, _TARGETS, _HOT = 0, 1, 2, 3, 4
 _GAIN_K, _WBAR, _TAU, _BIAS = 5, 6, 7, 8
 _DIR, _PH, _PW, _PT = 9, 10, 11, 12
+_ROT = 13
 # stream family of the structured inputs (make_profile_inputs)
 _PROFILE_ID = 100
 
@@ -199,8 +201,22 @@ def make_inputs(cfg: Config | str, seed: int = 0, *, K: Optional[int] = None, T:
     return out
 
 
+def random_orthogonal(rng: np.random.Generator, n: int, d: int) -> np.ndarray:
+    """n random d x d orthogonal matrices (Haar measure), fp64.
+
+    QR of a matrix of seeded standard normals, with the signs of R's diagonal
+    moved into Q so that the distribution does not depend on the QR routine's
+    sign convention.
+    """
+    out = np.empty((n, d, d), dtype=np.float64)
+    for i in range(n):
+        q, r = np.linalg.qr(rng.standard_normal((d, d)))
+        out[i] = q * np.where(np.diag(r) < 0, -1.0, 1.0)[None, :]
+    return out
+
+
 def make_extras(x: dict, seed: int = 0, *, per_module_gain: bool = False, wbar: str = "none",
-                tau: bool = False, bias: bool = False) -> dict:
+                tau: bool = False, bias: bool = False, rot: bool = False) -> dict:
     """Extra inputs of the general call for the workload ``x`` (from make_inputs).
 
     ``per_module_gain``: ``gain`` becomes [K, d], 1 + N(0, gain_sigma^2) per module.
@@ -208,9 +224,12 @@ def make_extras(x: dict, seed: int = 0, *, per_module_gain: bool = False, wbar: 
     an earlier step's copy or a shared random readout) or "per_head" ([K-1, V, d]).
     ``tau``: temperatures [K] uniform on [0.5, 2) (learned logit scales), fp32.
     ``bias``: biases [K, V], N(0, 0.5^2), fp32.
+    ``rot``: [K-1, d, d] random orthogonal matrices (the ROT variant's fixed
+    per-head bases), rounded once to the dtype (so only nearly orthogonal in bf16).
     Returns a dict with the same keys as make_inputs (``gain``, ``gain_bits``
-    replaced when per-module) plus ``Wbar`` (and ``Wbar_bits``), ``tau``, ``bias``
-    (None when absent).  Tensor values are exactly representable in the dtype.
+    replaced when per-module) plus ``Wbar`` (and ``Wbar_bits``), ``tau``, ``bias``,
+    ``rot`` (and ``rot_bits``) (None when absent).  Tensor values are exactly
+    representable in the dtype.
     """
     cfg = x["cfg"]
     K, d, V = cfg.K, cfg.d, cfg.V
@@ -234,6 +253,10 @@ def make_extras(x: dict, seed: int = 0, *, per_module_gain: bool = False, wbar: 
     out["tau"] = (np.float32(0.5) + np.float32(1.5) * _rng(seed, cfg.config_id, _TAU).random(K, dtype=np.float32)
                   ) if tau else None
     out["bias"] = _normal_f32(_rng(seed, cfg.config_id, _BIAS), (K, V), 0.5) if bias else None
+    out["rot"] = out["rot_bits"] = None
+    if rot:
+        r = random_orthogonal(_rng(seed, cfg.config_id, _ROT), max(K - 1, 0), d).astype(np.float32)
+        out["rot_bits"], out["rot"] = stored(r)
     return out
 
 

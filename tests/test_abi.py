@@ -37,7 +37,7 @@ def test_exports_match_header():
     out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
     exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
     assert set(names) <= exported
-    assert B.abi_version() == 2
+    assert B.abi_version() == 3
 
 
 def test_status_strings():
@@ -215,8 +215,18 @@ def test_general_workspace_sizes():
     assert B.exit_eval_workspace_size(gargs(readout_per_head=1, Wbar=P)) == 3 * al(kt * 4) + wt + al((K - 1) * tiled(V, d))
     # the vector-ALU family (fp32) reads the row-major readout: no tiled copies
     assert B.exit_eval_workspace_size(gargs(dtype=B.SOLO_F32)) == 3 * al(kt * 4)
+    # ROT: ones (d elements), the heads' rotated rows ((K-1) T d elements); fwd_bwd also
+    # e and D ((K-1) T d floats each) and the transposed rotations ((K-1) d^2 elements)
+    htd = (K - 1) * T * d
+    rot = al(d * 2) + al(htd * 2)
+    assert B.exit_eval_workspace_size(gargs(rot=P)) == 3 * al(kt * 4) + wt + rot
+    assert B.general_workspace_size(gargs(rot=P)) == head + rot + 2 * al(htd * 4) + al((K - 1) * d * d * 2)
+    assert B.exit_eval_workspace_size(gargs(rot=P, dtype=B.SOLO_F32)) == 3 * al(kt * 4) + al(d * 4) + al(htd * 4)
+    # one module has no head: rot is ignored
+    assert B.general_workspace_size(gargs(K=1, rot=P)) == B.general_workspace_size(gargs(K=1))
     # rejected flags -> 0
     assert B.general_workspace_size(gargs(gain_per_module=2)) == 0
+    assert B.general_workspace_size(gargs(rot=P, readout_per_head=1, Wbar=P)) == 0
     assert B.general_workspace_size(gargs(K=0)) == 0
 
 
@@ -228,6 +238,8 @@ def test_general_workspace_sizes():
     (dict(gain_per_module=3), "SOLO_ERR_ARG"),
     (dict(readout_per_head=1), "SOLO_ERR_ARG"),                       # per-head readout without Wbar
     (dict(heads_train_readout=1, Wbar=P), "SOLO_ERR_ARG"),            # PRIV without per-head readouts
+    (dict(rot=P, readout_per_head=1, Wbar=P), "SOLO_ERR_ARG"),        # ROT rotates one shared readout
+    (dict(rot=P + 8), "SOLO_ERR_ALIGN"),
     (dict(h=0), "SOLO_ERR_NULL"),
     (dict(dh=0), "SOLO_ERR_NULL"),
     (dict(dW=0), "SOLO_ERR_NULL"),

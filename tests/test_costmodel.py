@@ -89,6 +89,10 @@ def test_general_flops_special_cases():
     assert cm.executed_flops(K, T, V, d, heads_train_readout=True, bias_grad=True) == 4 * K * r2
     assert cm.executed_flops(K, T, V, d, final_module_dW=False, bias_grad=True) == 3 * K * r2
     assert cm.executed_flops(K, T, V, d, exit_eval=True) == K * r2
+    # ROT: the heads' rows rotated (2 T d^2 each), and their gradients rotated back
+    assert cm.executed_flops(K, T, V, d, rot=True) - cm.executed_flops(K, T, V, d) == 2 * (K - 1) * 2 * T * d * d
+    assert cm.executed_flops(K, T, V, d, rot=True, exit_eval=True) - K * r2 == (K - 1) * 2 * T * d * d
+    assert cm.executed_flops(1, T, V, d, rot=True) == cm.executed_flops(1, T, V, d)
     # 1B headline: 19.33 TFLOP algorithmic, 21.47 executed
     assert abs(cm.general_flops(K, T, V, d) / 1e12 - 19.33) < 0.01
     assert abs(cm.executed_flops(K, T, V, d) / 1e12 - 21.47) < 0.01

@@ -5,7 +5,8 @@ The general call's variants at the 1B and 340M shapes are checked in full
 against the general fp64 oracle, element by element: losses, per-token
 losses, every module's input gradient, the terminal's readout gradient, every
 head's readout gradient (PRIV), every module's gain gradient (per-module
-gains), temperature and bias gradients.  The exit evaluation's per-token
+gains), temperature and bias gradients; ROT against the oracle handed
+Wbar R_k as each head's readout.  The exit evaluation's per-token
 outputs (row losses, top-1) are checked on a seeded sample of token rows of
 every module against the oracle run on those rows alone, with bounds derived
 from the kernel's operand rounding; the module losses against the oracle's
@@ -91,6 +92,7 @@ VARIANTS = {
     "per_module_gain": (dict(per_module_gain=True), dict(final_module_dW=True)),
     "rand": (dict(wbar="per_head"), dict(final_module_dW=True)),
     "priv": (dict(wbar="per_head"), dict(final_module_dW=True, heads_train_readout=True)),
+    "rot": (dict(rot=True), dict(final_module_dW=True)),
 }
 
 

@@ -66,7 +66,7 @@ def _dev(x):
             return torch.from_numpy(np.ascontiguousarray(x[name + "_bits"]).view(np.int16)).view(torch.bfloat16).to(dev)
         return torch.from_numpy(np.ascontiguousarray(x[name])).to(dev)
 
-    f = {n: up(n) for n in ("h", "gain", "W", "Wbar")}
+    f = {n: up(n) for n in ("h", "gain", "W", "Wbar", "rot")}
     f["targets"] = torch.from_numpy(x["targets"]).to(dev)
     f["tau"] = torch.from_numpy(x["tau"]).to(dev) if x.get("tau") is not None else None
     f["bias"] = torch.from_numpy(x["bias"]).to(dev) if x.get("bias") is not None else None
@@ -80,12 +80,26 @@ def run_general(x, flags):
 
     f = _dev(x)
     out = binding.readout_general(f["h"], f["gain"], f["W"], f["targets"], Wbar=f["Wbar"], tau=f["tau"],
-                                  bias=f["bias"], row_loss=True, **flags)
+                                  bias=f["bias"], rot=f["rot"], row_loss=True, **flags)
     torch.cuda.synchronize()
     return {k: (None if v is None else v.double().cpu().numpy()) for k, v in out._asdict().items()}
 
 
+def oracle_view(x):
+    """The inputs as the oracle reads them.  ROT (head k reads Wbar R_k, with
+    Wbar = W when there is no separate copy): the oracle gets one readout per
+    head, the product formed here in fp64 from the stored values."""
+    if x.get("rot") is None:
+        return x
+    base = (x["W"] if x.get("Wbar") is None else x["Wbar"]).astype(np.float64)
+    xo = dict(x)
+    xo["rot"] = None
+    xo["Wbar"] = np.stack([base @ r.astype(np.float64) for r in x["rot"]])
+    return xo
+
+
 def oracle_general(x, flags):
+    x = oracle_view(x)
     return oracle.general_fwd_bwd(x["h"], x["gain"], x["W"], x["targets"], Wbar=x.get("Wbar"), tau=x.get("tau"),
                                   bias=x.get("bias"), final_module_dW=flags.get("final_module_dW", True),
                                   heads_train_readout=flags.get("heads_train_readout", False))
@@ -204,7 +218,8 @@ def run_exit_eval(x):
     from paper_2609_35440_amd import binding
 
     f = _dev(x)
-    out = binding.exit_eval(f["h"], f["gain"], f["W"], f["targets"], Wbar=f["Wbar"], tau=f["tau"], bias=f["bias"])
+    out = binding.exit_eval(f["h"], f["gain"], f["W"], f["targets"], Wbar=f["Wbar"], tau=f["tau"], bias=f["bias"],
+                            rot=f["rot"])
     torch.cuda.synchronize()
     return out.losses.double().cpu().numpy(), out.row_loss.double().cpu().numpy(), out.top1.cpu().numpy()
 

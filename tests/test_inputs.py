@@ -82,3 +82,24 @@ def test_hot_token_fraction():
 def test_config_table(name):
     cfg = CONFIGS[name]
     assert cfg.d % 8 == 0 and cfg.K >= 1 and cfg.T >= 1 and cfg.V >= 1
+
+
+def test_random_rotations():
+    # orthogonal to fp64 rounding before storage; rounded once to the dtype; seeded
+    from solo_inputs import make_extras, random_orthogonal
+
+    q = random_orthogonal(np.random.default_rng(0), 3, 64)
+    for r in q:
+        assert np.abs(r.T @ r - np.eye(64)).max() < 1e-12
+    x = make_extras(make_inputs("340m", seed=1, K=3, T=8, d=256, V=16), 1, rot=True)
+    r = x["rot"]
+    assert r.shape == (2, 256, 256) and r.dtype == np.float32
+    np.testing.assert_array_equal(r, round_bf16(r))
+    # bf16 storage keeps each R_k orthogonal to about 2^-8
+    for rk in r.astype(np.float64):
+        assert np.abs(rk.T @ rk - np.eye(256)).max() < 2e-2
+    y = make_extras(make_inputs("340m", seed=1, K=3, T=8, d=256, V=16), 1, rot=True)
+    np.testing.assert_array_equal(x["rot_bits"], y["rot_bits"])
+    z = make_extras(make_inputs("340m", seed=1, K=3, T=8, d=256, V=16), 2, rot=True)
+    assert not np.array_equal(x["rot_bits"], z["rot_bits"])
+    assert make_extras(make_inputs("340m", seed=1, K=3, T=8, d=256, V=16), 1)["rot"] is None
