@@ -21,75 +21,134 @@ using mfma::bf16x8;
 using mfma::f32x16;
 using mfma::f32x4;
 
-// C[m][n] = sum_k A[m][k] B[n][k] on 32x32x16 bf16 matrix instructions.  A
-// workgroup of 4 waves owns a 64 x 128 tile of C; wave (wm, wn) a 32 x 64
-// block (two products per 16-deep step).  Operands come straight from global
-// memory: lane l holds A[m0 + l % 32][k0 + 8 (l / 32) .. + 7] and
-// B[n0 + l % 32][k0 + 8 (l / 32) .. + 7], 16 contiguous bytes each.
+// C[m][n] = sum_k A[m][k] B[n][k] on 32x32x16 bf16 matrix instructions.
+// Workgroup tile 128 x 128 (4 waves, each a 64 x 64 block: 2 x 2 products of
+// 32 x 32), k in steps of 64 staged through LDS: each 16-byte granule of the
+// two 128 x 64 operand tiles is loaded by one thread into registers a step
+// ahead, then written to LDS, whose rows have a 144-byte pitch (8 lanes of a
+// 16-byte access, rows r..r+7 at one column, fall in 8 distinct 4-bank
+// groups).  Lane l of a product reads A[row l % 32][k + 8 (l / 32) .. + 7]
+// and B[col l % 32][same k].
 // AT: bf16 A (times a per-column gain, rounded once to bf16, when gain is not
-// null) or fp32 A (split into two bf16 parts); CT: bf16 or fp32 C.  N % 128 == 0,
-// K % 16 == 0; rows m >= M read as zero and are not written.
+// null) or fp32 A, split into two bf16 parts hi = bf16(x), lo = bf16(x - hi)
+// whose products both accumulate (about 16 bits of A; B is bf16 already).
+// CT: bf16 or fp32 C.  N % 128 == 0, K % 64 == 0; rows m >= M read as zero
+// and are not written.
+constexpr int GT = 128;          // tile rows and columns
+constexpr int GK = 64;           // k per staged step
+constexpr int GP = GK + 8;       // LDS row pitch in elements (144 bytes)
+
 template <typename AT, typename CT>
-__global__ __launch_bounds__(256) void k_gemm_nt_mfma(const AT* __restrict__ A, long long a_mat, const bf16* gain,
-                                                     int g_stride, const bf16* __restrict__ B, long long b_mat,
-                                                     CT* __restrict__ C, long long c_mat, int M, int N, int Kd) {
-    const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
+__global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const AT* __restrict__ A, long long a_mat,
+                                                        const bf16* __restrict__ gain, int g_stride,
+                                                        const bf16* __restrict__ B, long long b_mat,
+                                                        CT* __restrict__ C, long long c_mat, int M, int N, int Kd) {
+    constexpr bool SPLIT = sizeof(AT) == 4;
+    constexpr int NA = SPLIT ? 2 : 1;
+    __shared__ __attribute__((aligned(16))) bf16 As[NA][GT * GP];
+    __shared__ __attribute__((aligned(16))) bf16 Bs[GT * GP];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
     const int mat = blockIdx.z;
+    const int n0 = blockIdx.x * GT;
+    const int m0 = blockIdx.y * GT;
     A += mat * a_mat;
     B += mat * b_mat;
     C += mat * c_mat;
     const bf16* g = gain ? gain + (long long)mat * g_stride : nullptr;
-    const int m0 = blockIdx.x * 64 + 32 * (w & 1);
-    const int n0 = blockIdx.y * 128 + 64 * (w >> 1);
-    const int mr = m0 + (lane & 31);
-    const bool mok = mr < M;
-    const int kl = 8 * (lane >> 5);
-    f32x16 acc[2];
+
+    // staging: granule q = tid + 256 i (i < 4) of a tile is row q / 8, columns 8 (q % 8) .. + 7
+    const int kc = tid & 7;
+    bf16x8 bst[4];
+    bf16x8 ast[NA][4];
+    auto load = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+        for (int i = 0; i < 4; ++i) {
+            const int r = (tid >> 3) + 32 * i;
+            bst[i] = *(const bf16x8*)(B + (long long)(n0 + r) * Kd + k0 + 8 * kc);
+            const int m = m0 + r;
+            const bool ok = m < M;
+            if constexpr (SPLIT) {
+                f32x4 x0 = {0.f, 0.f, 0.f, 0.f}, x1 = x0;
+                if (ok) {
+                    x0 = *(const f32x4*)((const float*)A + (long long)m * Kd + k0 + 8 * kc);
+                    x1 = *(const f32x4*)((const float*)A + (long long)m * Kd + k0 + 8 * kc + 4);
+                }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[b][i] = 0.f;
-    for (int k0 = 0; k0 < Kd; k0 += 16) {
-        const int kk = k0 + kl;
-        bf16x8 av, alo;
-        if constexpr (sizeof(AT) == 2) {
-            av = mok ? *(const bf16x8*)((const bf16*)A + (long long)mr * Kd + kk) : bf16x8{};
-            if (g) {
-                const bf16x8 gv = *(const bf16x8*)(g + kk);
+                for (int e = 0; e < 8; ++e) {
+                    const float xv = e < 4 ? x0[e] : x1[e - 4];
+                    ast[0][i][e] = (bf16)xv;
+                    ast[NA - 1][i][e] = (bf16)(xv - (float)ast[0][i][e]);
+                }
+            } else {
+                bf16x8 av = {};
+                if (ok) av = *(const bf16x8*)((const bf16*)A + (long long)m * Kd + k0 + 8 * kc);
+                if (g) {
+                    const bf16x8 gv = *(const bf16x8*)(g + k0 + 8 * kc);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) av[e] = (bf16)((float)av[e] * (float)gv[e]);
-            }
-        } else {
-            // fp32 A as the sum of two bf16 parts, hi = bf16(x) and lo = bf16(x - hi):
-            // the product then keeps about 16 bits of A (B is bf16 already)
-            f32x4 x0 = {0.f, 0.f, 0.f, 0.f}, x1 = x0;
-            if (mok) {
-                x0 = *(const f32x4*)((const float*)A + (long long)mr * Kd + kk);
-                x1 = *(const f32x4*)((const float*)A + (long long)mr * Kd + kk + 4);
-            }
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float xv = e < 4 ? x0[e] : x1[e - 4];
-                av[e] = (bf16)xv;
-                alo[e] = (bf16)(xv - (float)av[e]);
+                    for (int e = 0; e < 8; ++e) av[e] = (bf16)((float)av[e] * (float)gv[e]);
+                }
+                ast[0][i] = av;
             }
         }
+    };
+    auto store = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            const bf16x8 bv = *(const bf16x8*)(B + (long long)(n0 + 32 * b + (lane & 31)) * Kd + kk);
-            acc[b] = mfma::mfma32(av, bv, acc[b]);
-            if constexpr (sizeof(AT) == 4) acc[b] = mfma::mfma32(alo, bv, acc[b]);
+        for (int i = 0; i < 4; ++i) {
+            const int off = ((tid >> 3) + 32 * i) * GP + 8 * kc;
+            *(bf16x8*)(Bs + off) = bst[i];
+#pragma unroll
+            for (int p = 0; p < NA; ++p) *(bf16x8*)(As[p] + off) = ast[p][i];
+        }
+    };
+
+    const int wm = 64 * (w & 1), wn = 64 * (w >> 1);
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[bi][bj][i] = 0.f;
+
+    load(0);
+    store();
+    __syncthreads();
+    const int ro = (lane & 31) * GP + 8 * (lane >> 5);
+    for (int k0 = 0; k0 < Kd; k0 += GK) {
+        const bool more = k0 + GK < Kd;
+        if (more) load(k0 + GK);  // in flight during this step's products
+#pragma unroll
+        for (int s = 0; s < GK / 16; ++s) {
+            bf16x8 bf[2];
+#pragma unroll
+            for (int bj = 0; bj < 2; ++bj) bf[bj] = *(const bf16x8*)(Bs + (wn + 32 * bj) * GP + ro + 16 * s);
+#pragma unroll
+            for (int p = 0; p < NA; ++p)
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi) {
+                    const bf16x8 af = *(const bf16x8*)(As[p] + (wm + 32 * bi) * GP + ro + 16 * s);
+#pragma unroll
+                    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = mfma::mfma32(af, bf[bj], acc[bi][bj]);
+                }
+        }
+        __syncthreads();
+        if (more) {
+            store();
+            __syncthreads();
         }
     }
-    // C layout: lane holds C[m0 + 8 (i / 4) + 4 (lane / 32) + i % 4][n0 + 32 b + lane % 32]
+    // C layout: lane holds C[8 (i / 4) + 4 (lane / 32) + i % 4][lane % 32] of each 32 x 32 block
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int m = m0 + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
-            if (m < M) C[(long long)m * N + n0 + 32 * b + (lane & 31)] = (CT)acc[b][i];
-        }
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int m = m0 + wm + 32 * bi + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+                if (m < M) C[(long long)m * N + n0 + wn + 32 * bj + (lane & 31)] = (CT)acc[bi][bj][i];
+            }
 }
 
 // The same product in fp32 on the vector ALU (fp32 storage, and bf16 widths
@@ -141,59 +200,86 @@ __global__ void k_fill_one(E* __restrict__ p, int n) {
 }
 
 // The RMSNorm backward of ROT heads from the rotated-back gradient D = e R_k
-// (fp32, [T][d] per head): dhhat = tau D, dn = g * dhhat, c = mean(dn * n),
+// (fp32, [T][d] per head): dhat = tau D, dn = g * dhat, c = mean(dn * n),
 // dh = r (dn - c n); with a per-module gain also the tile's partial sums of
-// dhhat * n (rows tiles of the local-loss pass).  One workgroup per tile of
-// rows rows of one head; thread t takes columns t + 256 q.
+// dhat * n (tiles of rows rows, those of the local-loss pass).  One workgroup
+// per tile of one head; wave w takes the tile's rows w, w + 4, ..., one row at
+// a time with lane l on columns 4 l + 256 q .. + 3 (a row's mean is a wave reduction:
+// no barrier inside the loop); the row is read twice, the second time from
+// cache.  Each wave sums its gain partials in its own LDS row; the four rows
+// meet in a fixed order at the end.
+typedef float V4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ V4 ld4(const float* p) { return *(const V4*)p; }
+__device__ __forceinline__ V4 ld4(const bf16* p) {
+    typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+    const b4 v = *(const b4*)p;
+    return V4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+__device__ __forceinline__ void st4(float* p, V4 v) { *(V4*)p = v; }
+__device__ __forceinline__ void st4(bf16* p, V4 v) {
+    typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+    *(b4*)p = b4{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+}
+
 template <typename E>
 __global__ __launch_bounds__(256) void k_rot_post(const float* __restrict__ D, const E* __restrict__ h,
                                                  const E* __restrict__ gain, int g_stride, const float* __restrict__ rstd,
                                                  const float* __restrict__ tau, E* __restrict__ dh, float* dgain_part,
                                                  int T, int d, int rows) {
-    constexpr int NQ = 16;  // d <= 4096
-    __shared__ float red[8];
+    extern __shared__ __attribute__((aligned(16))) float pbuf[];  // [4][d] when dgain_part is not null
     const int k = blockIdx.y;
     const int tile = blockIdx.x;
-    const int tid = threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
     const float tk = tau ? tau[k] : 1.f;
     const E* g = gain + (long long)k * g_stride;
-    float part[NQ];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) part[q] = 0.f;
-    for (int tr = 0; tr < rows; ++tr) {
+    float* pw = pbuf + w * d;
+    if (dgain_part)
+        for (int j = lane; j < d; j += 64) pw[j] = 0.f;
+    for (int tr = w; tr < rows; tr += 4) {
         const int t = tile * rows + tr;
         if (t >= T) break;
         const long long row = (long long)k * T + t;
         const float r = rstd[row];
+        const float* Dr = D + row * d;
+        const E* hr = h + row * d;
+        // four adjacent columns per lane and access (d % 8 == 0)
         float c = 0.f;
+#pragma unroll 4
+        for (int j = 4 * lane; j < d; j += 256) {
+            const f32x4 dv = *(const f32x4*)(Dr + j);
+            const V4 hv = ld4(hr + j), gv = ld4(g + j);
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int j = tid + 256 * q;
-            if (j < d) c = fmaf((float)g[j] * tk * D[row * d + j], r * (float)h[row * d + j], c);
+            for (int e = 0; e < 4; ++e) c = fmaf(gv[e] * (tk * dv[e]), r * hv[e], c);
         }
         for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
-        if ((tid & 63) == 0) red[tid >> 6] = c;
-        __syncthreads();
-        const float cm = (red[0] + red[1] + red[2] + red[3]) / (float)d;
-        __syncthreads();
+        const float cm = c / (float)d;
+        E* out = dh + row * d;
+#pragma unroll 4
+        for (int j = 4 * lane; j < d; j += 256) {
+            const f32x4 dv = *(const f32x4*)(Dr + j);
+            const V4 hv = ld4(hr + j), gv = ld4(g + j);
+            f32x4 o, pv;
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int j = tid + 256 * q;
-            if (j < d) {
-                const float dhat = tk * D[row * d + j];
-                const float n = r * (float)h[row * d + j];
-                dh[row * d + j] = (E)(r * ((float)g[j] * dhat - cm * n));
-                part[q] = fmaf(dhat, n, part[q]);
+            for (int e = 0; e < 4; ++e) {
+                const float dhat = tk * dv[e];
+                const float n = r * hv[e];
+                o[e] = r * (gv[e] * dhat - cm * n);
+                pv[e] = dhat * n;
+            }
+            st4(out + j, o);
+            if (dgain_part) {
+                f32x4 a = *(f32x4*)(pw + j);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) a[e] += pv[e];
+                *(f32x4*)(pw + j) = a;
             }
         }
     }
     if (dgain_part) {
+        __syncthreads();
         float* p = dgain_part + ((long long)k * gridDim.x + tile) * d;
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int j = tid + 256 * q;
-            if (j < d) p[j] = part[q];
-        }
+        for (int j = threadIdx.x; j < d; j += 256) p[j] = ((pbuf[j] + pbuf[d + j]) + pbuf[2 * d + j]) + pbuf[3 * d + j];
     }
 }
 
@@ -204,8 +290,8 @@ __global__ __launch_bounds__(256) void k_rot_post(const float* __restrict__ D, c
 hipError_t launch_rot_gemm(int dtype, bool a_f32, const void* A, long long a_mat, const void* gain, int g_stride,
                            const void* B, long long b_mat, void* C, bool c_f32, long long c_mat, int nmat, int M,
                            int N, int Kd, hipStream_t s) {
-    if (dtype == 0 && N % 128 == 0 && Kd % 16 == 0) {
-        dim3 grid((unsigned)((M + 63) / 64), (unsigned)(N / 128), (unsigned)nmat);
+    if (dtype == 0 && N % GT == 0 && Kd % GK == 0) {
+        dim3 grid((unsigned)(N / GT), (unsigned)((M + GT - 1) / GT), (unsigned)nmat);
         if (!a_f32 && !c_f32)
             hipLaunchKernelGGL((k_gemm_nt_mfma<bf16, bf16>), grid, dim3(256), 0, s, (const bf16*)A, a_mat,
                                (const bf16*)gain, g_stride, (const bf16*)B, b_mat, (bf16*)C, c_mat, M, N, Kd);
@@ -255,11 +341,12 @@ hipError_t launch_rot_post(int dtype, const float* D, const void* h, const void*
                            const float* rstd, const float* tau, void* dh, float* dgain_part, int nmod, int T, int d,
                            int rows, hipStream_t s) {
     dim3 grid((unsigned)((T + rows - 1) / rows), (unsigned)nmod);
+    const size_t lds = dgain_part ? (size_t)4 * d * 4 : 0;
     if (dtype == 0)
-        hipLaunchKernelGGL(k_rot_post<bf16>, grid, dim3(256), 0, s, D, (const bf16*)h, (const bf16*)gain, g_stride,
+        hipLaunchKernelGGL(k_rot_post<bf16>, grid, dim3(256), lds, s, D, (const bf16*)h, (const bf16*)gain, g_stride,
                            rstd, tau, (bf16*)dh, dgain_part, T, d, rows);
     else
-        hipLaunchKernelGGL(k_rot_post<float>, grid, dim3(256), 0, s, D, (const float*)h, (const float*)gain,
+        hipLaunchKernelGGL(k_rot_post<float>, grid, dim3(256), lds, s, D, (const float*)h, (const float*)gain,
                            g_stride, rstd, tau, (float*)dh, dgain_part, T, d, rows);
     return hipGetLastError();
 }
