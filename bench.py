@@ -210,7 +210,8 @@ def main(argv=None) -> int:
     ap.add_argument("--cpu-sample-tokens", type=int, default=8192,
                     help="tokens per module of the oracle's bounded sample (0 to skip)")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic_local_loss_1b.json"),
-                    help="HBM traffic of the dominant kernel measured with rocprofv3 counters (JSON), if present")
+                    help="fabric traffic (L2 to memory system) of the dominant kernel measured with rocprofv3 "
+                         "counters (JSON), if present")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device copy of MIB MiB a few times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -418,8 +419,11 @@ def main(argv=None) -> int:
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
+            # counter-measured bytes per launch between the L2 and the memory system
+            # (Infinity Cache hits included, so an upper bound on DRAM bytes)
             "traffic": traffic,
-            "hbm_gb_per_s": (traffic / (ll_ms / 1e3) / 1e9) if traffic else None,
+            "traffic_kind": "fabric",
+            "fabric_gb_per_s": (traffic / (ll_ms / 1e3) / 1e9) if traffic else None,
             "algorithmic_flops_per_launch": ll_flops,
             "launch_ms": ll_ms,
         },
