@@ -15,9 +15,11 @@
 // transposing reads of the 16x16x16 second product spread their 8-byte
 // pieces over all 64 banks when G = 40.
 //
-// The chunk is staged through registers: lane p of staged load q fetches
-// granule slot 64 q + p of the slice in row-major order (row-contiguous
-// global reads) and writes it to its swizzled LDS place.
+// The chunk reaches LDS from registers: the passes with a second product
+// load the logit product's operand straight from the tiled readout copy
+// (lane l: row l % 16, granule 4 kk + l / 16 at k-step kk) and write those
+// registers to the place a row-wise read of that operand would address
+// (rowread_off), where the transposing reads find them.
 #pragma once
 
 #if defined(__HIPCC__)
@@ -36,7 +38,6 @@ template <int DS>
 struct Geo {
     static constexpr int G = DS / 8;          // granules per row of a wave slice
     static constexpr int SLOTS = YC * G;      // granules per slice
-    static constexpr int NI = SLOTS / 64;     // staged 1 KiB loads per slice
     static constexpr int SLICE = YC * DS * 2;  // bytes of one wave's chunk slice
     static_assert(G % 8 == 0 && SLOTS % 64 == 0, "slice width: a multiple of 64 columns");
 };
@@ -45,21 +46,6 @@ struct Geo {
 template <int DS>
 SOLO_HDW int phys(int r, int g) {
     return 16 * (r * Geo<DS>::G + (g ^ (r & 7)));
-}
-
-// staged load q, lane p: the row and granule it fetches ...
-template <int DS>
-SOLO_HDW int stage_row(int q, int p) {
-    return (64 * q + p) / Geo<DS>::G;
-}
-template <int DS>
-SOLO_HDW int stage_gran(int q, int p) {
-    return (64 * q + p) % Geo<DS>::G;
-}
-// ... and where it goes in LDS
-template <int DS>
-SOLO_HDW int stage_dst(int q, int p) {
-    return phys<DS>(stage_row<DS>(q, p), stage_gran<DS>(q, p));
 }
 
 // row-wise operand read at k-step kk: lane l, row l % 16, granule 4 kk + l / 16
