@@ -187,6 +187,24 @@ def test_args_struct_layout_matches_header(tmp_path):
     assert int(got["size"]) == ctypes.sizeof(B.SoloReadoutArgs)
 
 
+def test_status_values_match_header(tmp_path):
+    # the numbering of solo_status as the C compiler sees it (SOLO_ERR_ARG = 6 and
+    # SOLO_ERR_HIP = 7 are this boundary's own choice) against the binding's table
+    names = sorted(B.STATUS)
+    src = tmp_path / "status.c"
+    body = "\n".join(f'    printf("{n} %d\\n", (int){n});' for n in names)
+    src.write_text('#include <stdio.h>\n#include "solo_readout.h"\nint main(void) {\n'
+                   f'{body}\n    printf("ABI %d\\n", SOLO_READOUT_ABI_VERSION);\n    return 0;\n}}\n')
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    exe = tmp_path / "status"
+    subprocess.run(["gcc", "-std=c99", f"-I{inc}", str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines())
+    for n in names:
+        assert int(got[n]) == B.STATUS[n], n
+    assert B.STATUS["SOLO_ERR_ARG"] == 6 and B.STATUS["SOLO_ERR_HIP"] == 7
+    assert int(got["ABI"]) == B.abi_version()
+
+
 def test_general_workspace_sizes():
     K, T, d, V = 3, 40, 256, 100
     kt = K * T
