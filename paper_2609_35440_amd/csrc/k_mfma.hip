@@ -597,15 +597,23 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused(FusedArgs a) {
             const float cmean = tau_k * csum / (float)d;
             if (a.rowdtau && w == 0 && ehh == 0 && xok[h]) a.rowdtau[modoff + xg] = tok[h] ? csum : 0.f;
             if (a.ebuf) {
-                // e to the buffer; the RMSNorm backward follows the rotation back
+                // e to the buffer as bf16 planes hi | lo; the RMSNorm backward follows
+                // the rotation back
                 if (xok[h]) {
+                    bf16* er = (bf16*)a.ebuf + (modoff + xg) * (long long)(2 * d);
 #pragma unroll
                     for (int b = 0; b < (PC ? G::NB : 1); ++b)
 #pragma unroll
                         for (int i4 = 0; i4 < 4; ++i4) {
-                            const f32x4 o = {acc[b][h][4 * i4], acc[b][h][4 * i4 + 1], acc[b][h][4 * i4 + 2],
-                                             acc[b][h][4 * i4 + 3]};
-                            *(f32x4*)(a.ebuf + (modoff + xg) * (long long)d + js + 32 * b + 8 * i4 + 4 * ehh) = o;
+                            const int j = js + 32 * b + 8 * i4 + 4 * ehh;
+                            mfma::bf16x4 hi, lo;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                hi[e] = (bf16)acc[b][h][4 * i4 + e];
+                                lo[e] = (bf16)(acc[b][h][4 * i4 + e] - (float)hi[e]);
+                            }
+                            *(mfma::bf16x4*)(er + j) = hi;
+                            *(mfma::bf16x4*)(er + d + j) = lo;
                         }
                 }
                 continue;

@@ -434,9 +434,19 @@ __global__ __launch_bounds__(NTHR, 1) void k_fused_wide(FusedArgs a) {
         // sweep 2: dh = r (dn - c n); or e to the buffer, whose RMSNorm backward
         // follows the rotation back (ROT heads)
         if (xok && a.ebuf) {
+            bf16* er = (bf16*)a.ebuf + (modoff + xg) * (long long)(2 * d);
 #pragma unroll
-            for (int b = 0; b < G::NB; ++b)
-                *(f32x4*)(a.ebuf + (modoff + xg) * (long long)d + js + 16 * b + 4 * eg) = acc[b];
+            for (int b = 0; b < G::NB; ++b) {
+                const int j = js + 16 * b + 4 * eg;
+                bf16x4w hi, lo;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    hi[e] = (bf16)acc[b][e];
+                    lo[e] = (bf16)(acc[b][e] - (float)hi[e]);
+                }
+                *(bf16x4w*)(er + j) = hi;
+                *(bf16x4w*)(er + d + j) = lo;
+            }
         }
         if (xok && !a.ebuf) {
             bf16* dhrow = (bf16*)a.dh + (modoff + xg) * (long long)d;

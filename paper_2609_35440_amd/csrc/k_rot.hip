@@ -10,7 +10,8 @@
 //
 // with r_t, n_t = r_t h_t of the original hidden states (the rotation commutes
 // with the row scale r_t).  Both products are C = A B^T of row-major A [M][K]
-// and B [N][K]: u = (g * h) R_k^T and dhhat / tau = e (R_k^T)^T.
+// and B [N][K]: u = (g * h) R_k^T and dhhat / tau = e (R_k^T)^T, the latter
+// with e as two bf16 planes (hi | lo, a 2d-deep row) on the matrix cores.
 #include "mfma_common.h"
 
 namespace solo {
@@ -21,92 +22,76 @@ using mfma::bf16x8;
 using mfma::f32x16;
 using mfma::f32x4;
 
-// C[m][n] = sum_k A[m][k] B[n][k] on 32x32x16 bf16 matrix instructions.
-// Workgroup tile 128 x 128 (4 waves, each a 64 x 64 block: 2 x 2 products of
-// 32 x 32), k in steps of 64 staged through LDS: each 16-byte granule of the
-// two 128 x 64 operand tiles is loaded by one thread into registers a step
-// ahead, then written to LDS, whose rows have a 144-byte pitch (8 lanes of a
-// 16-byte access, rows r..r+7 at one column, fall in 8 distinct 4-bank
-// groups).  Lane l of a product reads A[row l % 32][k + 8 (l / 32) .. + 7]
-// and B[col l % 32][same k].
-// AT: bf16 A (times a per-column gain, rounded once to bf16, when gain is not
-// null) or fp32 A, split into two bf16 parts hi = bf16(x), lo = bf16(x - hi)
-// whose products both accumulate (about 16 bits of A; B is bf16 already).
-// CT: bf16 or fp32 C.  N % 128 == 0, K % 64 == 0; rows m >= M read as zero
-// and are not written.
-constexpr int GT = 128;          // tile rows and columns
+// C[m][n] = sum_k A[m][k] B[n][k mod ldb] on 32x32x16 bf16 matrix
+// instructions, A [M][Kd] and B [N][ldb] row-major bf16 (Kd = ldb, or
+// Kd = 2 ldb for the rotate-back product, whose A rows are e's two bf16
+// planes hi | lo and whose B is then read twice).  Workgroup tile 256 x 128
+// (4 waves, each a 128 x 64 block: 4 x 2 products of 32 x 32), k in steps of
+// 64 staged through LDS: each 16-byte granule of the 256 x 64 and 128 x 64
+// operand tiles is loaded by one thread into registers a step ahead, then
+// written to LDS, whose rows have a 144-byte pitch (8 lanes of a 16-byte
+// access, rows r..r+7 at one column, fall in 8 distinct 4-bank groups).  Lane
+// l of a product reads A[row l % 32][k + 8 (l / 32) .. + 7] and B[col l % 32][same k].
+// With a gain, A is bf16(A * gain[k]) (the rounding of the local-loss pass's
+// stationary tile).  CT: bf16 or fp32 C.  N % 128 == 0, ldb % 64 == 0;
+// rows m >= M read as zero and are not written.
+constexpr int GM = 256;          // tile rows
+constexpr int GN = 128;          // tile columns
 constexpr int GK = 64;           // k per staged step
 constexpr int GP = GK + 8;       // LDS row pitch in elements (144 bytes)
 
-template <typename AT, typename CT>
-__global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const AT* __restrict__ A, long long a_mat,
+template <typename CT>
+__global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const bf16* __restrict__ A, long long a_mat, int Kd,
                                                         const bf16* __restrict__ gain, int g_stride,
-                                                        const bf16* __restrict__ B, long long b_mat,
-                                                        CT* __restrict__ C, long long c_mat, int M, int N, int Kd) {
-    constexpr bool SPLIT = sizeof(AT) == 4;
-    constexpr int NA = SPLIT ? 2 : 1;
-    __shared__ __attribute__((aligned(16))) bf16 As[NA][GT * GP];
-    __shared__ __attribute__((aligned(16))) bf16 Bs[GT * GP];
+                                                        const bf16* __restrict__ B, long long b_mat, int ldb,
+                                                        CT* __restrict__ C, long long c_mat, int M, int N) {
+    __shared__ __attribute__((aligned(16))) bf16 As[GM * GP];
+    __shared__ __attribute__((aligned(16))) bf16 Bs[GN * GP];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
     const int mat = blockIdx.z;
-    const int n0 = blockIdx.x * GT;
-    const int m0 = blockIdx.y * GT;
+    const int n0 = blockIdx.x * GN;
+    const int m0 = blockIdx.y * GM;
     A += mat * a_mat;
     B += mat * b_mat;
     C += mat * c_mat;
     const bf16* g = gain ? gain + (long long)mat * g_stride : nullptr;
 
-    // staging: granule q = tid + 256 i (i < 4) of a tile is row q / 8, columns 8 (q % 8) .. + 7
+    // staging: granule q = tid + 256 i of a tile is row q / 8, columns 8 (q % 8) .. + 7
     const int kc = tid & 7;
-    bf16x8 bst[4];
-    bf16x8 ast[NA][4];
+    const int r0 = tid >> 3;
+    bf16x8 ast[GM / 32], bst[GN / 32];
     auto load = [&](int k0) __attribute__((always_inline)) {
+        const int kb = k0 >= ldb ? k0 - ldb : k0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            bst[i] = *(const bf16x8*)(B + (long long)(n0 + r) * Kd + k0 + 8 * kc);
-            const int m = m0 + r;
-            const bool ok = m < M;
-            if constexpr (SPLIT) {
-                f32x4 x0 = {0.f, 0.f, 0.f, 0.f}, x1 = x0;
-                if (ok) {
-                    x0 = *(const f32x4*)((const float*)A + (long long)m * Kd + k0 + 8 * kc);
-                    x1 = *(const f32x4*)((const float*)A + (long long)m * Kd + k0 + 8 * kc + 4);
-                }
+        for (int i = 0; i < GN / 32; ++i)
+            bst[i] = *(const bf16x8*)(B + (long long)(n0 + r0 + 32 * i) * ldb + kb + 8 * kc);
+        bf16x8 gv = {};
+        if (g) gv = *(const bf16x8*)(g + k0 + 8 * kc);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float xv = e < 4 ? x0[e] : x1[e - 4];
-                    ast[0][i][e] = (bf16)xv;
-                    ast[NA - 1][i][e] = (bf16)(xv - (float)ast[0][i][e]);
-                }
-            } else {
-                bf16x8 av = {};
-                if (ok) av = *(const bf16x8*)((const bf16*)A + (long long)m * Kd + k0 + 8 * kc);
-                if (g) {
-                    const bf16x8 gv = *(const bf16x8*)(g + k0 + 8 * kc);
+        for (int i = 0; i < GM / 32; ++i) {
+            const int m = m0 + r0 + 32 * i;
+            bf16x8 av = {};
+            if (m < M) av = *(const bf16x8*)(A + (long long)m * Kd + k0 + 8 * kc);
+            if (g) {
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) av[e] = (bf16)((float)av[e] * (float)gv[e]);
-                }
-                ast[0][i] = av;
+                for (int e = 0; e < 8; ++e) av[e] = (bf16)((float)av[e] * (float)gv[e]);
             }
+            ast[i] = av;
         }
     };
     auto store = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int off = ((tid >> 3) + 32 * i) * GP + 8 * kc;
-            *(bf16x8*)(Bs + off) = bst[i];
+        for (int i = 0; i < GN / 32; ++i) *(bf16x8*)(Bs + (r0 + 32 * i) * GP + 8 * kc) = bst[i];
 #pragma unroll
-            for (int p = 0; p < NA; ++p) *(bf16x8*)(As[p] + off) = ast[p][i];
-        }
+        for (int i = 0; i < GM / 32; ++i) *(bf16x8*)(As + (r0 + 32 * i) * GP + 8 * kc) = ast[i];
     };
 
-    const int wm = 64 * (w & 1), wn = 64 * (w >> 1);
-    f32x16 acc[2][2];
+    const int wm = 128 * (w & 1), wn = 64 * (w >> 1);
+    f32x16 acc[4][2];
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
@@ -125,13 +110,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const AT* __restrict__ 
 #pragma unroll
             for (int bj = 0; bj < 2; ++bj) bf[bj] = *(const bf16x8*)(Bs + (wn + 32 * bj) * GP + ro + 16 * s);
 #pragma unroll
-            for (int p = 0; p < NA; ++p)
+            for (int bi = 0; bi < 4; ++bi) {
+                const bf16x8 af = *(const bf16x8*)(As + (wm + 32 * bi) * GP + ro + 16 * s);
 #pragma unroll
-                for (int bi = 0; bi < 2; ++bi) {
-                    const bf16x8 af = *(const bf16x8*)(As[p] + (wm + 32 * bi) * GP + ro + 16 * s);
-#pragma unroll
-                    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = mfma::mfma32(af, bf[bj], acc[bi][bj]);
-                }
+                for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = mfma::mfma32(af, bf[bj], acc[bi][bj]);
+            }
         }
         __syncthreads();
         if (more) {
@@ -141,7 +124,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const AT* __restrict__ 
     }
     // C layout: lane holds C[8 (i / 4) + 4 (lane / 32) + i % 4][lane % 32] of each 32 x 32 block
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int bi = 0; bi < 4; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
@@ -285,38 +268,45 @@ __global__ __launch_bounds__(256) void k_rot_post(const float* __restrict__ D, c
 
 }  // namespace
 
-// C = A B^T per matrix (nmat of them, strides in elements): A bf16 (times
-// gain) or fp32, B in the storage dtype, C bf16/fp32 as named.
-hipError_t launch_rot_gemm(int dtype, bool a_f32, const void* A, long long a_mat, const void* gain, int g_stride,
-                           const void* B, long long b_mat, void* C, bool c_f32, long long c_mat, int nmat, int M,
-                           int N, int Kd, hipStream_t s) {
-    if (dtype == 0 && N % GT == 0 && Kd % GK == 0) {
-        dim3 grid((unsigned)(N / GT), (unsigned)((M + GT - 1) / GT), (unsigned)nmat);
-        if (!a_f32 && !c_f32)
-            hipLaunchKernelGGL((k_gemm_nt_mfma<bf16, bf16>), grid, dim3(256), 0, s, (const bf16*)A, a_mat,
-                               (const bf16*)gain, g_stride, (const bf16*)B, b_mat, (bf16*)C, c_mat, M, N, Kd);
-        else if (a_f32 && c_f32)
-            hipLaunchKernelGGL((k_gemm_nt_mfma<float, float>), grid, dim3(256), 0, s, (const float*)A, a_mat,
-                               (const bf16*)gain, g_stride, (const bf16*)B, b_mat, (float*)C, c_mat, M, N, Kd);
-        else
-            return hipErrorInvalidValue;
+bool rot_back_planes(int dtype, int d) { return dtype == 0 && d % GN == 0 && d % GK == 0; }
+
+hipError_t launch_rot_rows(int dtype, const void* h, const void* gain, int g_stride, const void* R, void* u,
+                           int nmat, int T, int d, hipStream_t s) {
+    const long long td = (long long)T * d, dd = (long long)d * d;
+    if (rot_back_planes(dtype, d)) {
+        dim3 grid((unsigned)(d / GN), (unsigned)((T + GM - 1) / GM), (unsigned)nmat);
+        hipLaunchKernelGGL(k_gemm_nt_mfma<bf16>, grid, dim3(256), 0, s, (const bf16*)h, td, d, (const bf16*)gain,
+                           g_stride, (const bf16*)R, dd, d, (bf16*)u, td, T, d);
         return hipGetLastError();
     }
-    const long long n = (long long)M * N;
+    const long long n = td;
     dim3 grid((unsigned)((n + 255) / 256), 1, (unsigned)nmat);
-    if (dtype == 0) {
-        if (!a_f32 && !c_f32)
-            hipLaunchKernelGGL((k_gemm_nt_valu<bf16, bf16, bf16>), grid, dim3(256), 0, s, (const bf16*)A, a_mat,
-                               (const bf16*)gain, g_stride, (const bf16*)B, b_mat, (bf16*)C, c_mat, M, N, Kd);
-        else if (a_f32 && c_f32)
-            hipLaunchKernelGGL((k_gemm_nt_valu<float, bf16, float>), grid, dim3(256), 0, s, (const float*)A, a_mat,
-                               (const bf16*)gain, g_stride, (const bf16*)B, b_mat, (float*)C, c_mat, M, N, Kd);
-        else
-            return hipErrorInvalidValue;
-    } else {
-        hipLaunchKernelGGL((k_gemm_nt_valu<float, float, float>), grid, dim3(256), 0, s, (const float*)A, a_mat,
-                           (const float*)gain, g_stride, (const float*)B, b_mat, (float*)C, c_mat, M, N, Kd);
+    if (dtype == 0)
+        hipLaunchKernelGGL((k_gemm_nt_valu<bf16, bf16, bf16>), grid, dim3(256), 0, s, (const bf16*)h, td,
+                           (const bf16*)gain, g_stride, (const bf16*)R, dd, (bf16*)u, td, T, d, d);
+    else
+        hipLaunchKernelGGL((k_gemm_nt_valu<float, float, float>), grid, dim3(256), 0, s, (const float*)h, td,
+                           (const float*)gain, g_stride, (const float*)R, dd, (float*)u, td, T, d, d);
+    return hipGetLastError();
+}
+
+hipError_t launch_rot_back(int dtype, bool planes, const void* e, const void* Rt, float* D, int nmat, int T, int d,
+                           hipStream_t s) {
+    const long long td = (long long)T * d, dd = (long long)d * d;
+    if (planes) {
+        if (!rot_back_planes(dtype, d)) return hipErrorInvalidValue;
+        dim3 grid((unsigned)(d / GN), (unsigned)((T + GM - 1) / GM), (unsigned)nmat);
+        hipLaunchKernelGGL(k_gemm_nt_mfma<float>, grid, dim3(256), 0, s, (const bf16*)e, 2 * td, 2 * d,
+                           (const bf16*)nullptr, 0, (const bf16*)Rt, dd, d, D, td, T, d);
+        return hipGetLastError();
     }
+    dim3 grid((unsigned)((td + 255) / 256), 1, (unsigned)nmat);
+    if (dtype == 0)
+        hipLaunchKernelGGL((k_gemm_nt_valu<float, bf16, float>), grid, dim3(256), 0, s, (const float*)e, td,
+                           (const bf16*)nullptr, 0, (const bf16*)Rt, dd, D, td, T, d, d);
+    else
+        hipLaunchKernelGGL((k_gemm_nt_valu<float, float, float>), grid, dim3(256), 0, s, (const float*)e, td,
+                           (const float*)nullptr, 0, (const float*)Rt, dd, D, td, T, d, d);
     return hipGetLastError();
 }
 

@@ -292,7 +292,7 @@ __global__ __launch_bounds__(NTHR) void k_fused_valu(FusedArgs a) {
 #pragma unroll
                 for (int q = 0; q < NQ; ++q) {
                     const int j = tid + NTHR * q;
-                    if (j < d) a.ebuf[(modoff + xg) * (long long)d + j] = acc[r][q];
+                    if (j < d) ((float*)a.ebuf)[(modoff + xg) * (long long)d + j] = acc[r][q];
                 }
                 continue;
             }

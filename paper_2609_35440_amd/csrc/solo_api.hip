@@ -41,7 +41,8 @@ struct Plan {
     size_t rstd = 0, lse = 0, rowloss = 0, rowrec = 0, rowdtau = 0, dgp = 0, hg = 0;
     size_t wtile = 0, whtile = 0, total = 0;
     // ROT pieces: a vector of ones (the rotated rows' gain), the rotated rows
-    // u, the heads' e = sum_v delta_v Wbar_v (fp32), D = e R_k (fp32), R_k^T
+    // u, the heads' e = sum_v delta_v Wbar_v (4 bytes per element: two bf16
+    // planes, or fp32 on the vector-ALU family), D = e R_k (fp32), R_k^T
     size_t ones = 0, ubuf = 0, ebuf = 0, dbuf = 0, rtr = 0;
 };
 
@@ -253,13 +254,12 @@ int run(const solo_readout_args& x, bool eval) {
     solo::FusedArgs ah = a;
     if (P.rot) {
         if (solo::launch_fill_one(dt, ws + P.ones, d, s) != hipSuccess) return SOLO_ERR_HIP;
-        if (solo::launch_rot_gemm(dt, false, x.h, (long long)T * d, x.gain, a.g_stride, x.rot, (long long)d * d,
-                                  ws + P.ubuf, false, (long long)T * d, K - 1, T, d, d, s) != hipSuccess)
+        if (solo::launch_rot_rows(dt, x.h, x.gain, a.g_stride, x.rot, ws + P.ubuf, K - 1, T, d, s) != hipSuccess)
             return SOLO_ERR_HIP;
         ah.h = ws + P.ubuf;
         ah.gain = ws + P.ones;
         ah.g_stride = 0;
-        ah.ebuf = eval ? nullptr : (float*)(ws + P.ebuf);
+        ah.ebuf = eval ? nullptr : (void*)(ws + P.ebuf);
     }
     if (!mark(0)) return SOLO_ERR_HIP;
     // one launch over modules [m0, m0 + n) of a pass, with the arguments g
@@ -296,8 +296,8 @@ int run(const solo_readout_args& x, bool eval) {
         // back to the basis of h: D = e R_k = e (R_k^T)^T, then the heads' RMSNorm
         // backward (and their gain partials when every module trains its gain)
         if (solo::launch_transpose(dt, x.rot, ws + P.rtr, K - 1, d, s) != hipSuccess ||
-            solo::launch_rot_gemm(dt, true, ws + P.ebuf, (long long)T * d, nullptr, 0, ws + P.rtr, (long long)d * d,
-                                  ws + P.dbuf, true, (long long)T * d, K - 1, T, d, d, s) != hipSuccess ||
+            solo::launch_rot_back(dt, P.mfma, ws + P.ebuf, ws + P.rtr, (float*)(ws + P.dbuf), K - 1, T, d, s) !=
+                hipSuccess ||
             solo::launch_rot_post(dt, (const float*)(ws + P.dbuf), x.h, x.gain, a.g_stride, (const float*)(ws + P.rstd),
                                   x.tau, x.dh, P.dg_mode == 2 ? a.dgain_part : nullptr, K - 1, T, d, P.rows,
                                   s) != hipSuccess)

@@ -62,9 +62,12 @@ struct FusedArgs {
     float* dWt;           // [V][d] or null: d loss_{K-1} / d W
     float* dWh;           // [K-1][V][d] or null: d loss_k / d readout_k of the heads
     float* dbias;         // [K][V] or null: d loss_k / d b_k
-    float* ebuf;          // [..][T][d] or null: the local-loss pass writes e_t = sum_v delta_tv R_kv (fp32,
-                          // module k at ebuf + k T d) instead of the RMSNorm backward (ROT heads: their
-                          // stationary rows are rotated states, whose gradient is rotated back afterwards)
+    void* ebuf;           // null, or: the local-loss pass writes e_t = sum_v delta_tv R_kv there instead of
+                          // the RMSNorm backward (ROT heads: their stationary rows are rotated states, whose
+                          // gradient is rotated back afterwards).  Row m = k T + t holds 4 d bytes: the
+                          // matrix-core families write two bf16 planes, hi = bf16(e) at [0, d) and
+                          // lo = bf16(e - hi) at [d, 2d) (the rotate-back product's operand as a 2d-deep
+                          // bf16 row); the vector-ALU family writes e in fp32
 };
 
 // Tile sizes of the two kernel families (the workspace depends on them).
@@ -106,9 +109,14 @@ hipError_t launch_local_loss_valu(int dtype, const FusedArgs& a, int nmod, hipSt
 hipError_t launch_exit_eval_valu(int dtype, const FusedArgs& a, int nmod, hipStream_t s);
 // ROT (k_rot.hip): C = A B^T per matrix; transposes; a vector of ones; the
 // heads' RMSNorm backward from the rotated-back gradient D = e R_k
-hipError_t launch_rot_gemm(int dtype, bool a_f32, const void* A, long long a_mat, const void* gain, int g_stride,
-                           const void* B, long long b_mat, void* C, bool c_f32, long long c_mat, int nmat, int M,
-                           int N, int Kd, hipStream_t s);
+// u[m] = bf16(R_m bf16(g_m * h_m)) per row, heads m < nmat (gain g_m at gain + m g_stride)
+hipError_t launch_rot_rows(int dtype, const void* h, const void* gain, int g_stride, const void* R, void* u,
+                           int nmat, int T, int d, hipStream_t s);
+// D[m] = e_m R_m from R_m^T (Rt); e as the matrix-core families' bf16 planes or in fp32
+hipError_t launch_rot_back(int dtype, bool planes, const void* e, const void* Rt, float* D, int nmat, int T, int d,
+                           hipStream_t s);
+// whether launch_rot_back takes the planes form at this dtype and width
+bool rot_back_planes(int dtype, int d);
 hipError_t launch_transpose(int dtype, const void* in, void* out, int nmat, int d, hipStream_t s);
 hipError_t launch_fill_one(int dtype, void* p, int n, hipStream_t s);
 hipError_t launch_rot_post(int dtype, const float* D, const void* h, const void* gain, int g_stride,
