@@ -4,7 +4,7 @@
 // rotates the head's normalised states instead of forming the V x d product:
 //
 //   u_t     = R_k (g_k * h_t)                  (bf16, the head's stationary rows)
-//   e_t     = sum_v delta_tv Wbar_v / tau_k    (the local-loss pass on u)
+//   e_t     = sum_v delta_tv Wbar_v            (the local-loss pass on u)
 //   dhhat_t = tau_k R_k^T e_t                  (back to the hidden states' basis)
 //   dh_t    = r_t (g_k * dhhat_t - c_t n_t),  c_t = mean_j g_kj dhhat_tj n_tj
 //
