@@ -34,7 +34,8 @@ using mfma::f32x4;
 // l of a product reads A[row l % 32][k + 8 (l / 32) .. + 7] and B[col l % 32][same k].
 // With a gain, A is bf16(A * gain[k]) (the rounding of the local-loss pass's
 // stationary tile).  CT: bf16 or fp32 C.  N % 128 == 0, ldb % 64 == 0;
-// rows m >= M read as zero and are not written.
+// rows m >= M read as zero and are not written.  Row tile of workgroup
+// (x, y, z): mtile0 + y (launches of at most 65535 row tiles).
 constexpr int GM = 256;          // tile rows
 constexpr int GN = 128;          // tile columns
 constexpr int GK = 64;           // k per staged step
@@ -44,7 +45,8 @@ template <typename CT>
 __global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const bf16* __restrict__ A, long long a_mat, int Kd,
                                                         const bf16* __restrict__ gain, int g_stride,
                                                         const bf16* __restrict__ B, long long b_mat, int ldb,
-                                                        CT* __restrict__ C, long long c_mat, int M, int N) {
+                                                        CT* __restrict__ C, long long c_mat, int M, int N,
+                                                        int mtile0) {
     __shared__ __attribute__((aligned(16))) bf16 As[GM * GP];
     __shared__ __attribute__((aligned(16))) bf16 Bs[GN * GP];
     const int tid = threadIdx.x;
@@ -52,7 +54,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_nt_mfma(const bf16* __restrict_
     const int w = tid >> 6;
     const int mat = blockIdx.z;
     const int n0 = blockIdx.x * GN;
-    const int m0 = blockIdx.y * GM;
+    const int m0 = (mtile0 + (int)blockIdx.y) * GM;
     A += mat * a_mat;
     B += mat * b_mat;
     C += mat * c_mat;
@@ -270,24 +272,44 @@ __global__ __launch_bounds__(256) void k_rot_post(const float* __restrict__ D, c
 
 bool rot_back_planes(int dtype, int d) { return dtype == 0 && d % GN == 0 && d % GK == 0; }
 
+// the matrix-core product over all row tiles, in launches of at most 65535 of them
+template <typename CT>
+hipError_t gemm_mfma(const bf16* A, long long a_mat, int Kd, const bf16* gain, int g_stride, const bf16* B,
+                     long long b_mat, int ldb, CT* C, long long c_mat, int nmat, int M, int N, hipStream_t s) {
+    const int mtiles = (M + GM - 1) / GM;
+    for (int t0 = 0; t0 < mtiles; t0 += 65535) {
+        const int nt = mtiles - t0 < 65535 ? mtiles - t0 : 65535;
+        dim3 grid((unsigned)(N / GN), (unsigned)nt, (unsigned)nmat);
+        hipLaunchKernelGGL(k_gemm_nt_mfma<CT>, grid, dim3(256), 0, s, A, a_mat, Kd, gain, g_stride, B, b_mat, ldb, C,
+                           c_mat, M, N, t0);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// the vector-ALU product, one thread per element of C
+template <typename AT, typename BT, typename CT>
+hipError_t gemm_valu(const AT* A, long long a_mat, const BT* gain, int g_stride, const BT* B, long long b_mat, CT* C,
+                     long long c_mat, int nmat, int M, int N, int Kd, hipStream_t s) {
+    const long long blocks = ((long long)M * N + 255) / 256;
+    if (blocks > 2147483647LL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_gemm_nt_valu<AT, BT, CT>), dim3((unsigned)blocks, 1, (unsigned)nmat), dim3(256), 0, s, A,
+                       a_mat, gain, g_stride, B, b_mat, C, c_mat, M, N, Kd);
+    return hipGetLastError();
+}
+
 hipError_t launch_rot_rows(int dtype, const void* h, const void* gain, int g_stride, const void* R, void* u,
                            int nmat, int T, int d, hipStream_t s) {
     const long long td = (long long)T * d, dd = (long long)d * d;
-    if (rot_back_planes(dtype, d)) {
-        dim3 grid((unsigned)(d / GN), (unsigned)((T + GM - 1) / GM), (unsigned)nmat);
-        hipLaunchKernelGGL(k_gemm_nt_mfma<bf16>, grid, dim3(256), 0, s, (const bf16*)h, td, d, (const bf16*)gain,
-                           g_stride, (const bf16*)R, dd, d, (bf16*)u, td, T, d);
-        return hipGetLastError();
-    }
-    const long long n = td;
-    dim3 grid((unsigned)((n + 255) / 256), 1, (unsigned)nmat);
+    if (rot_back_planes(dtype, d))
+        return gemm_mfma<bf16>((const bf16*)h, td, d, (const bf16*)gain, g_stride, (const bf16*)R, dd, d, (bf16*)u,
+                               td, nmat, T, d, s);
     if (dtype == 0)
-        hipLaunchKernelGGL((k_gemm_nt_valu<bf16, bf16, bf16>), grid, dim3(256), 0, s, (const bf16*)h, td,
-                           (const bf16*)gain, g_stride, (const bf16*)R, dd, (bf16*)u, td, T, d, d);
-    else
-        hipLaunchKernelGGL((k_gemm_nt_valu<float, float, float>), grid, dim3(256), 0, s, (const float*)h, td,
-                           (const float*)gain, g_stride, (const float*)R, dd, (float*)u, td, T, d, d);
-    return hipGetLastError();
+        return gemm_valu<bf16, bf16, bf16>((const bf16*)h, td, (const bf16*)gain, g_stride, (const bf16*)R, dd,
+                                           (bf16*)u, td, nmat, T, d, d, s);
+    return gemm_valu<float, float, float>((const float*)h, td, (const float*)gain, g_stride, (const float*)R, dd,
+                                          (float*)u, td, nmat, T, d, d, s);
 }
 
 hipError_t launch_rot_back(int dtype, bool planes, const void* e, const void* Rt, float* D, int nmat, int T, int d,
@@ -295,19 +317,14 @@ hipError_t launch_rot_back(int dtype, bool planes, const void* e, const void* Rt
     const long long td = (long long)T * d, dd = (long long)d * d;
     if (planes) {
         if (!rot_back_planes(dtype, d)) return hipErrorInvalidValue;
-        dim3 grid((unsigned)(d / GN), (unsigned)((T + GM - 1) / GM), (unsigned)nmat);
-        hipLaunchKernelGGL(k_gemm_nt_mfma<float>, grid, dim3(256), 0, s, (const bf16*)e, 2 * td, 2 * d,
-                           (const bf16*)nullptr, 0, (const bf16*)Rt, dd, d, D, td, T, d);
-        return hipGetLastError();
+        return gemm_mfma<float>((const bf16*)e, 2 * td, 2 * d, nullptr, 0, (const bf16*)Rt, dd, d, D, td, nmat, T, d,
+                                s);
     }
-    dim3 grid((unsigned)((td + 255) / 256), 1, (unsigned)nmat);
     if (dtype == 0)
-        hipLaunchKernelGGL((k_gemm_nt_valu<float, bf16, float>), grid, dim3(256), 0, s, (const float*)e, td,
-                           (const bf16*)nullptr, 0, (const bf16*)Rt, dd, D, td, T, d, d);
-    else
-        hipLaunchKernelGGL((k_gemm_nt_valu<float, float, float>), grid, dim3(256), 0, s, (const float*)e, td,
-                           (const float*)nullptr, 0, (const float*)Rt, dd, D, td, T, d, d);
-    return hipGetLastError();
+        return gemm_valu<float, bf16, float>((const float*)e, td, nullptr, 0, (const bf16*)Rt, dd, D, td, nmat, T, d,
+                                             d, s);
+    return gemm_valu<float, float, float>((const float*)e, td, nullptr, 0, (const float*)Rt, dd, D, td, nmat, T, d, d,
+                                          s);
 }
 
 hipError_t launch_transpose(int dtype, const void* in, void* out, int nmat, int d, hipStream_t s) {
