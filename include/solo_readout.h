@@ -158,9 +158,11 @@ int solo_readout_fwd_bwd(int K, int T, int d, int V, int dtype, float eps,
  * previous event when the stage has no work in this call.
  */
 #define SOLO_NUM_STAGES 6
-/*   0  per-token inverse RMS of h                                           */
+/*   0  per-token inverse RMS of h (and the tiled readout copies; with rot, */
+/*      the heads' rotated rows)                                             */
 /*   1  local-loss pass (logits, online log-sum-exp, dh; all K), or the     */
-/*      forward-only exit evaluation                                         */
+/*      forward-only exit evaluation; with rot also the heads' gradient     */
+/*      rotated back and their RMSNorm backward                              */
 /*   2  per-module sums in fixed order: losses, temperature gradients        */
 /*   3  readout-gradient pass (modules whose readout is trained), after the */
 /*      gain-scaled copy of h the matrix-core gradient passes stream         */
