@@ -10,8 +10,9 @@
 //
 //   local-loss pass (every module; Eq. 2 and Eq. 3):
 //     stationary X = XR rows t of g_k * h_k, streamed Y = the readout rows v,
-//     online (max, sum-exp) per row, and acc_t += sum_v exp(z_tv - m_t) R_kv,
-//     so that dhhat_t = tau_k (acc_t / s_t - R_{k,y_t}) / T at the end, followed
+//     online (max, sum-exp) per row, and acc_t += sum_{v != y_t} exp(z_tv - m_t) R_kv,
+//     so that dhhat_t = tau_k (acc_t / s_t + (p_{t,y} - 1) R_{k,y_t}) / T at the
+//     end (the target's whole entry of delta in fp32, see finish_row), followed
 //     by the RMSNorm backward and, for a module that trains its gain, the
 //     tile's partial of dgain = sum_t dhhat_t * n_t.  The T x V logits and
 //     probabilities stay on chip.
@@ -43,12 +44,11 @@
 // with the transposing read for the second product.  The passes without one
 // (exit evaluation, bias gradient) stream the tiled copy of Y (see
 // tiled_elems) straight into the registers that feed the logit product, one
-// contiguous 1 KiB per wave and instruction, and need no LDS for the chunk.
-// (Measured at d = 2048: exit evaluation 9.22 -> 8.09 ms, the heads'
-// bias-gradient pass 7.23 -> 6.46 ms.  With a second product the registers
-// still have to be written to LDS for the transposing read, and those
-// ds_write_b128 cost more than the direct-to-LDS stream and the row-wise
-// reads together: local-loss pass 18.0 -> 20.6 ms.)
+// contiguous 1 KiB per wave and instruction, and need no LDS for the chunk,
+// which measured faster at d = 2048.  With a second product the registers
+// would still have to be written to LDS for the transposing read, and those
+// ds_write_b128 measured slower than the direct-to-LDS stream and the
+// row-wise reads together at d = 2048, so those passes keep the stream.
 #include "mfma_common.h"
 
 namespace solo {
