@@ -109,3 +109,35 @@ def test_fullsize_general_variant_in_full(name, variant):
     ref = oracle_general(x, flags)
     log(f"{name} {variant}: oracle done")
     compare(g, ref, cfg.dtype, flags, f"{name} {variant} (full)")
+
+
+def test_fullsize_rot_2b_wide():
+    """ROT at the 2B shape (the wide family; seven rotated heads and the
+    terminal as separate launches): every head's per-token losses and input
+    gradients on seeded row samples against the oracle handed W R_k (formed in
+    fp64) as that head's readout, with the module's full T in the mean; the
+    terminal module (loss, dh, dW, dgain) in full."""
+    from tests.gpu_helpers import check_close
+
+    x = make_extras(make_inputs("2b", seed=0), 0, rot=True)
+    cfg = x["cfg"]
+    log(f"full-size ROT 2b: K={cfg.K} T={cfg.T} d={cfg.d} V={cfg.V}")
+    g = run_general(x, dict(final_module_dW=True))
+    for key, v in g.items():
+        if v is not None:
+            assert np.all(np.isfinite(v)), key
+    tol = TOL[cfg.dtype]
+    W64 = x["W"].astype(np.float64)
+    for k in range(cfg.K - 1):
+        rows = _sample(cfg.T, 400 + k)
+        Wk = W64 @ x["rot"][k].astype(np.float64)
+        rl, dh, _, _ = oracle.module_fwd_bwd(x["h"][k, rows], x["targets"][k, rows], Wk, x["gain"], T_total=cfg.T)
+        e_rl = np.abs(g["row_loss"][k, rows] - rl).max() / max(1.0, np.abs(rl).max())
+        e_dh = rel_max_err(g["dh"][k, rows], dh)
+        log(f"rot 2b head {k}: sampled rows {len(rows)}, row_loss err {e_rl:.2e}, dh err {e_dh:.2e}")
+        assert e_rl <= 2 * tol["loss"] and e_dh <= tol["grad"], (k, e_rl, e_dh)
+    kf = cfg.K - 1
+    rl, dh, dW, dgain = oracle.module_fwd_bwd(x["h"][kf], x["targets"][kf], x["W"], x["gain"], want_readout_grads=True)
+    ref = {"losses": np.array([rl.mean()]), "dh": dh[None], "dW": dW, "dgain": dgain}
+    gk = {"losses": g["losses"][kf:], "dh": g["dh"][kf:], "dW": g["dW"], "dgain": g["dgain"]}
+    check_close(gk, ref, cfg.dtype, what="rot 2b terminal module (full)")
