@@ -372,6 +372,7 @@ def main(argv=None) -> int:
     ll_flops = (1 if is_eval else 2) * 2 * K * T * V * d
     achieved = ll_flops / (ll_ms / 1e3) / 1e12
     traffic = None
+    mfma_busy = None  # counter-measured busy fraction of the matrix units in that kernel
     if os.path.exists(args.traffic):
         try:
             with open(args.traffic) as f:
@@ -380,8 +381,9 @@ def main(argv=None) -> int:
             if (tr.get("config") == args.config and tr.get("family") == family and args.variant == "headline"
                     and tr.get("kernel_sources_sha256_16") == kernel_sources_hash()):
                 traffic = tr.get("bytes_per_launch")
+                mfma_busy = tr.get("mfma_busy")
         except Exception:
-            traffic = None
+            traffic = mfma_busy = None
 
     result = {
         "metric": METRIC,
@@ -424,6 +426,7 @@ def main(argv=None) -> int:
             "traffic": traffic,
             "traffic_kind": "fabric",
             "fabric_gb_per_s": (traffic / (ll_ms / 1e3) / 1e9) if traffic else None,
+            "mfma_busy_counter": mfma_busy,
             "algorithmic_flops_per_launch": ll_flops,
             "launch_ms": ll_ms,
         },
