@@ -31,6 +31,10 @@ CASES = [
     ("wide_d2560_all", "2b", dict(K=3, T=37, d=2560, V=300), ALL_ROT, ALL_FLAGS),
     ("valu_f32_all", "tiny", dict(K=3, T=37, d=24, V=45), ALL_ROT, ALL_FLAGS),
     ("valu_bf16_d72_all", "340m", dict(K=2, T=10, d=72, V=50), ALL_ROT, ALL_FLAGS),
+    # vector-ALU passes at a width whose rotation products run on the matrix cores
+    ("valu_bf16_d3072_all", "1b", dict(K=2, T=20, d=3072, V=40), ALL_ROT, ALL_FLAGS),
+    ("valu_f32_d256", "tiny", dict(K=3, T=21, d=256, V=30), dict(tau=True, rot=True),
+     dict(final_module_dW=True, want_dtau=True)),
 ]
 
 
