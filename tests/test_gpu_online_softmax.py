@@ -8,7 +8,10 @@ paths, for every kernel family:
   - rows whose target holds nearly all of the probability (16 nats above the
     rest), placed in the first chunk or in the last one, with a strong
     competitor early in the vocabulary: the input gradient's (p_y - 1) R_y
-    term is then a small difference of large numbers.
+    term is then a small difference of large numbers;
+  - logits of magnitude about 80 everywhere (between 72 and 80 nats), where
+    the fp32 log-sum-exp carries a large offset and the spread still
+    triggers an occasional re-base.
 
 The inputs come from solo_inputs.make_profile_inputs (readout rows that share
 a direction with the hidden states); fwd_bwd (losses, dh, dW, dgain) and the
@@ -43,6 +46,10 @@ def _profile(kind):
         c[20] = 8.0                                                    # strong competitor in chunk 1
         t[0] = 5
         t[1] = np.where(np.arange(T) % 2 == 0, 5, rng.integers(0, V, T))
+    elif kind == "high":
+        c = (72.0 + 8.0 * np.modf(v * 0.6180339887)[0]).astype(np.float32)
+        t[0] = rng.integers(0, V, T)
+        t[1] = rng.integers(0, V, T)
     elif kind == "peak_last":
         c[3] = 9.0                                                     # strong competitor in chunk 0
         c[V - 2] = 16.0
@@ -53,7 +60,7 @@ def _profile(kind):
     return c, t
 
 
-@pytest.mark.parametrize("kind", ["climb", "peak_first", "peak_last"])
+@pytest.mark.parametrize("kind", ["climb", "peak_first", "peak_last", "high"])
 @pytest.mark.parametrize("fam,dtype,d", FAMILIES, ids=[f[0] for f in FAMILIES])
 def test_online_softmax_fwd_bwd(fam, dtype, d, kind):
     from paper_2609_35440_amd import binding
@@ -67,6 +74,12 @@ def test_online_softmax_fwd_bwd(fam, dtype, d, kind):
     ref = oracle.readout_fwd_bwd(x["h"], x["gain"], x["W"], x["targets"], True)
     log(f"{kind} {fam}: losses gpu {g['losses']} oracle {ref['losses']}")
     tol = TOL[dtype]
+    # gradients: the dtype's tolerance, or, where the logits are large, what fp32
+    # itself allows there: a probability's relative error is the absolute error
+    # of its logit, about sqrt(d) roundings of 2^-24 |z| in the dot product (and
+    # one of the log-sum-exp at that magnitude); 4 sqrt(d) 2^-24 max|z| covers it
+    zmax = float(np.abs(c).max()) + 1.0
+    gtol = max(tol["grad"], 4.0 * np.sqrt(d) * 2.0 ** -24 * zmax)
     errs = {}
     for k in range(K):
         # per-token losses within the bound derived from the operand rounding and
@@ -80,14 +93,14 @@ def test_online_softmax_fwd_bwd(fam, dtype, d, kind):
         errs[f"loss{k}"] = lerr / abs(ref["losses"][k])
         assert lerr <= max(tol["loss"] * abs(ref["losses"][k]), bound.mean()), (k, lerr, ref["losses"][k])
         errs[f"dh{k}"] = e = rel_max_err(g["dh"][k], ref["dh"][k])
-        assert e <= tol["grad"], ("dh", k, e)
+        assert e <= gtol, ("dh", k, e, gtol)
     for key in ("dW", "dgain"):
         errs[key] = e = rel_max_err(g[key], ref[key])
-        assert e <= tol["grad"], (key, e)
+        assert e <= gtol, (key, e, gtol)
     log(f"{kind} {fam}: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
 
 
-@pytest.mark.parametrize("kind", ["climb", "peak_first", "peak_last"])
+@pytest.mark.parametrize("kind", ["climb", "peak_first", "peak_last", "high"])
 @pytest.mark.parametrize("fam,dtype,d", FAMILIES, ids=[f[0] for f in FAMILIES])
 def test_online_softmax_exit_eval(fam, dtype, d, kind):
     import torch
