@@ -73,3 +73,50 @@ def test_noalloc_refuses_calls_beyond_the_scratch():
     assert st == binding.STATUS["SOLO_ERR_WORKSPACE"]
     torch.cuda.synchronize()
     assert (losses.cpu() == 7.0).all()   # nothing was enqueued
+
+
+def test_noalloc_under_graph_capture():
+    """What the entry point is for: a call captured into a HIP graph (nothing is
+    allocated inside the capture; the scratch address was fetched by an earlier
+    eager call) and replayed gives the eager call's bits on every replay, with
+    the program's own eager work and synchronisations between the replays."""
+    import torch
+
+    from paper_2609_35440_amd import binding
+
+    x = make_inputs("1b", seed=71, K=2, T=100, d=2048, V=500)
+    h, gain, W, targets = to_device(x)
+    K, T, d = h.shape
+    V = W.shape[0]
+    dev = h.device
+    out = {"losses": torch.empty(K, dtype=torch.float32, device=dev),
+           "row_loss": torch.empty((K, T), dtype=torch.float32, device=dev),
+           "dh": torch.empty_like(h),
+           "dW": torch.empty((V, d), dtype=torch.float32, device=dev),
+           "dgain": torch.empty(d, dtype=torch.float32, device=dev)}
+
+    def call(stream):
+        return binding.readout_fwd_bwd_noalloc_raw(
+            K, T, d, V, binding.SOLO_BF16, 1e-6, h.data_ptr(), gain.data_ptr(), W.data_ptr(), targets.data_ptr(), 1,
+            out["losses"].data_ptr(), out["row_loss"].data_ptr(), out["dh"].data_ptr(), out["dW"].data_ptr(),
+            out["dgain"].data_ptr(), stream.cuda_stream)
+
+    assert call(torch.cuda.current_stream()) == 0
+    torch.cuda.synchronize()
+    eager = {k: v.clone() for k, v in out.items()}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        st = call(side)
+    assert st == 0, binding.status_string(st)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for v in out.values():
+            v.fill_(float("nan"))  # the program's own eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for key, v in out.items():
+            assert torch.equal(v, eager[key]), (rep, key)
+        log(f"graph replay {rep}: outputs equal the eager call's")
