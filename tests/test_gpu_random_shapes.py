@@ -84,6 +84,38 @@ def test_random_general_parity(name, ov, extras, flags):
     compare(g, ref, x["cfg"].dtype, flags, name)
 
 
+def _rot_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = [256, 1024, 2048, 2560, 72, 1536][i % 6]  # both matrix-core tilings, vector-ALU bf16
+        K = int(rng.integers(2, 5))
+        T = int(rng.integers(1, 90))
+        V = int(rng.integers(1, 400))
+        extras = dict(per_module_gain=bool(rng.random() < 0.5), tau=bool(rng.random() < 0.5),
+                      bias=bool(rng.random() < 0.5), wbar=str(rng.choice(["none", "shared"])), rot=True)
+        if extras["wbar"] == "none":
+            extras.pop("wbar")
+        flags = dict(final_module_dW=bool(rng.random() < 0.75), want_dtau=bool(rng.random() < 0.5),
+                     want_dbias=bool(rng.random() < 0.5))
+        out.append((f"r{i}_K{K}_T{T}_d{d}_V{V}", dict(K=K, T=T, d=d, V=V), extras, flags))
+    return out
+
+
+ROT_CASES = _rot_cases(8, 31)
+
+
+@pytest.mark.parametrize("name,ov,extras,flags", ROT_CASES, ids=[c[0] for c in ROT_CASES])
+def test_random_rot_parity(name, ov, extras, flags):
+    # ROT: the oracle is handed W R_k (or the shared copy's) as each head's readout
+    cfg = "2b" if ov["d"] == 2560 else "1b"
+    x = make_extras(make_inputs(cfg, seed=zlib.crc32(name.encode()) % 1000, **ov), 7, **extras)
+    log(f"rot case {name}: extras {extras} flags {flags}")
+    g = run_general(x, flags)
+    ref = oracle_general(x, flags)
+    compare(g, ref, x["cfg"].dtype, flags, name)
+
+
 def _eval_cases(n, seed):
     rng = np.random.default_rng(seed)
     out = []
