@@ -130,3 +130,21 @@ def test_rot_exit_eval(name, cfg, ov, extras):
     # the forward of the training call computes the same losses
     g = run_general(x, dict(final_module_dW=False))
     np.testing.assert_allclose(losses, g["losses"], rtol=1e-6, err_msg=name)
+
+
+@pytest.mark.parametrize("cfg,ov", [("1b", dict(K=3, T=45, d=2048, V=300)), ("2b", dict(K=2, T=30, d=2560, V=90))],
+                         ids=["mfma", "wide"])
+def test_rot_needs_no_orthogonality(cfg, ov):
+    """The library applies R_k forward and R_k^T backward as given (the gradient
+    of <Wbar_v R_k, hhat> is R_k^T Wbar_v^T, whatever R_k is), so a matrix that
+    is far from orthogonal (Gaussian entries of variance 1/d) must match the
+    oracle handed Wbar R_k just as well."""
+    from solo_inputs import bf16_bits, bf16_from_bits
+
+    x = make_extras(make_inputs(cfg, seed=47, **ov), 47, tau=True, per_module_gain=True, rot=True)
+    K, d = x["cfg"].K, x["cfg"].d
+    r = (np.random.default_rng(47).standard_normal((K - 1, d, d)) / np.sqrt(d)).astype(np.float32)
+    x["rot_bits"] = bf16_bits(r)
+    x["rot"] = bf16_from_bits(x["rot_bits"])
+    flags = dict(final_module_dW=True, want_dtau=True)
+    compare(run_general(x, flags), oracle_general(x, flags), x["cfg"].dtype, flags, f"rot {cfg} gaussian R")
