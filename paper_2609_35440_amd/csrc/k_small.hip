@@ -95,15 +95,17 @@ __global__ void k_gain_rows(const bf16* __restrict__ h, long long src_stride, co
 // out[k] = scale * sum_t rows[k][t], fixed order, fp64 accumulation
 // (module losses: the per-token losses with scale 1/T; temperature gradients:
 // the per-token shares with scale 1).
-__global__ void k_module_sum(const float* __restrict__ rows, float* __restrict__ out, int T, double scale) {
-    __shared__ double red[256];
+__global__ __launch_bounds__(1024) void k_module_sum(const float* __restrict__ rows, float* __restrict__ out, int T,
+                                                    double scale) {
+    __shared__ double red[1024];
     const int k = blockIdx.x;
     const float* r = rows + (long long)k * T;
     double acc = 0.0;
-    for (int t = threadIdx.x; t < T; t += 256) acc += (double)r[t];
+#pragma unroll 8
+    for (int t = threadIdx.x; t < T; t += 1024) acc += (double)r[t];
     red[threadIdx.x] = acc;
     __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
+    for (int w = 512; w > 0; w >>= 1) {
         if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
         __syncthreads();
     }
@@ -120,8 +122,10 @@ __global__ void k_dgain_reduce(const float* __restrict__ part, float* __restrict
     part += (long long)blockIdx.y * ntiles * d;
     dgain += (long long)blockIdx.y * d;
     double acc = 0.0;
-    if (j < d)
+    if (j < d) {
+#pragma unroll 8
         for (int i = grp; i < ntiles; i += 8) acc += (double)part[(long long)i * d + j];
+    }
     red[grp][jl] = acc;
     __syncthreads();
     if (grp == 0 && j < d) {
@@ -162,7 +166,7 @@ hipError_t launch_gain_rows(const bf16* h, long long src_stride, const bf16* gai
 }
 
 hipError_t launch_module_sum(const float* rows, float* out, int K, int T, double scale, hipStream_t s) {
-    hipLaunchKernelGGL(k_module_sum, dim3(K), dim3(256), 0, s, rows, out, T, scale);
+    hipLaunchKernelGGL(k_module_sum, dim3(K), dim3(1024), 0, s, rows, out, T, scale);
     return hipGetLastError();
 }
 
