@@ -141,3 +141,32 @@ def test_fullsize_rot_2b_wide():
     ref = {"losses": np.array([rl.mean()]), "dh": dh[None], "dW": dW, "dgain": dgain}
     gk = {"losses": g["losses"][kf:], "dh": g["dh"][kf:], "dW": g["dW"], "dgain": g["dgain"]}
     check_close(gk, ref, cfg.dtype, what="rot 2b terminal module (full)")
+
+
+def test_fullsize_rot_exit_eval_1b():
+    """ROT through the exit evaluation at the 1B shape (the forward-only
+    register-fed pass on the rotated rows): sampled rows' losses and top-1
+    against the oracle handed W R_k, and module losses equal to the training
+    call's on the same inputs (the same forward on another tiling)."""
+    import torch
+
+    from paper_2609_35440_amd import binding
+    from tests.test_gpu_general import oracle_view, run_exit_eval
+
+    x = make_extras(make_inputs("1b", seed=0), 0, rot=True)
+    cfg = x["cfg"]
+    losses, row_loss, top1 = run_exit_eval(x)
+    assert np.all(np.isfinite(row_loss))
+    np.testing.assert_allclose(row_loss.mean(axis=1), losses, rtol=2e-6)
+    g = run_general(x, dict(final_module_dW=False))
+    np.testing.assert_allclose(losses, g["losses"], rtol=1e-5)
+    torch.cuda.empty_cache()
+    rows = _sample(cfg.T, 500)
+    xo = oracle_view(x)
+    ref = oracle.exit_eval(x["h"][:, rows], x["gain"], x["W"], x["targets"][:, rows], Wbar=xo["Wbar"])
+    tol = TOL[cfg.dtype]
+    rscale = max(np.abs(ref["row_loss"]).max(), 1.0)
+    err = np.abs(row_loss[:, rows] - ref["row_loss"]).max()
+    log(f"rot exit eval 1b: sampled rows {len(rows)}, row_loss err {err:.2e}")
+    assert err <= 2 * tol["loss"] * rscale, err
+    _check_top1(top1[:, rows], ref, cfg.V, cfg.dtype, "rot exit eval 1b")
